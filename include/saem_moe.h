@@ -1,0 +1,229 @@
+/*
+ * saem_moe.h -- C ABI of libsaem_moe.so: one MoE layer's forward on MI355X (gfx950).
+ *
+ * The operations follow SAEM (arXiv 2608.21614):
+ *   - top-k gating by a router (Section II-A);
+ *   - expert-aligned token repacking: the (token, expert) pairs of a batch are
+ *     grouped by expert into contiguous buffers, using only index reordering
+ *     and a workspace allocated once and reused across layers (Section IV-E.1,
+ *     Section VI-A);
+ *   - partition of the repacked batch by the residency map into GPU-bound rows
+ *     and a packed list of host-bound rows (Section IV-D.2), over a fixed set of
+ *     per-layer expert slots (Section IV-C.1, IV-C.2);
+ *   - one batched execution per resident expert (Section IV-E.1) on the matrix
+ *     cores (Section IV-D.2);
+ *   - a merge of the expert outputs back to token order (Section IV-D.2).
+ * The expert MLP is SwiGLU without biases: y = (silu(x W1) * (x W3)) W2.
+ *
+ * Conventions for every call
+ *   - Returns moe_status.  No exception or abort crosses the ABI.
+ *   - All tensor pointers are DEVICE pointers owned by the caller.  The library
+ *     never allocates or frees device memory and never synchronises the stream.
+ *   - Work is enqueued on `stream` (a hipStream_t; NULL is the null stream).
+ *   - Arguments are validated on the host before anything is enqueued; a call
+ *     that returns an error has enqueued nothing.  Validation never touches
+ *     device memory, so it works on a machine without a GPU.
+ *   - Kernel faults surface at the caller's next synchronisation, as usual for
+ *     HIP; launch failures return MOE_ERR_HIP.
+ *   - Calls on distinct streams with distinct workspaces may run concurrently.
+ *   - Every tensor pointer must be 16-byte aligned (MOE_ERR_INVALID_ARG otherwise).
+ *   - Layouts are row-major and K-contiguous:
+ *       x          [T, H]        activations (dims.dtype)
+ *       w_router   [E, H]        row e scores expert e (dims.dtype)
+ *       bias       [E]           fp32 router bias, or NULL
+ *       w13        [slots, 2F, H] per slot: rows 0..F-1 are the gate projection W1
+ *                                (row f = output feature f), rows F..2F-1 the up
+ *                                projection W3
+ *       w2         [slots, H, F] per slot: row h = output feature h of W2
+ *       ws13, ws2  [S, 2Fs, H], [S, H, Fs] shared experts, same layout
+ *   - Residency map: expert_slot[E] (int32, device).  Expert e is resident iff
+ *     0 <= expert_slot[e] < dims.slots, and then its weights are
+ *     w13[expert_slot[e]] and w2[expert_slot[e]]; any other value (e.g. -1)
+ *     means offloaded.
+ *   - A routed pair q = t*k + j is the j-th selected expert of token t.
+ *   - Packed rows: the pairs of resident experts first, experts in ascending id,
+ *     then the pairs of offloaded experts, experts in ascending id; inside an
+ *     expert, ascending token.  n_res = number of resident pairs, so rows
+ *     [0, n_res) are GPU-bound and rows [n_res, T*k) form the offloaded list.
+ */
+#ifndef SAEM_MOE_H
+#define SAEM_MOE_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define MOE_ABI_VERSION 1
+
+typedef enum moe_status {
+    MOE_OK = 0,
+    MOE_ERR_INVALID_ARG = 1,  /* NULL pointer, negative size, k > E, bad struct_size, ... */
+    MOE_ERR_UNSUPPORTED = 2,  /* valid but not supported: H or F not a multiple of 64, E > 256, k > 8 */
+    MOE_ERR_WORKSPACE = 3,    /* workspace NULL or smaller than moe_workspace_bytes() */
+    MOE_ERR_HIP = 4           /* a HIP launch or runtime call failed */
+} moe_status;
+
+typedef enum moe_dtype {
+    MOE_F32 = 0,   /* IEEE fp32 */
+    MOE_BF16 = 1   /* bfloat16 (fp32 accumulation everywhere) */
+} moe_dtype;
+
+/* Shapes of one MoE layer. */
+typedef struct moe_dims {
+    int32_t tokens;      /* T >= 0; T == 0 is a valid no-op that writes n_res = 0 */
+    int32_t hidden;      /* H >= 64, multiple of 64 */
+    int32_t experts;     /* E routed experts, 1..256 */
+    int32_t ffn;         /* F >= 64, multiple of 64 (routed expert width) */
+    int32_t top_k;       /* k, 1..min(E, 8) */
+    int32_t shared;      /* S >= 0 always-on shared experts (at most 8) */
+    int32_t shared_ffn;  /* Fs, multiple of 64 when S > 0, ignored when S == 0 */
+    int32_t slots;       /* number of resident-expert slots held in w13 / w2, 0..E */
+    int32_t dtype;       /* moe_dtype of x, w_router, w13, w2, ws13, ws2 */
+} moe_dims;
+
+/* flags of moe_route_topk and moe_layer_forward */
+#define MOE_LOGITS_IN 1u   /* route the caller's scores in `logits`; x and w_router are not read */
+
+int moe_abi_version(void);
+
+/* Static description of a status code. */
+const char* moe_status_str(moe_status s);
+
+/* Host-only validation of a shape description. */
+moe_status moe_check_dims(const moe_dims* dims);
+
+/*
+ * Bytes of workspace any call below needs for these dims (Section IV-E.1: the
+ * repacking workspace is allocated once and reused across all MoE layers).
+ * One workspace sized for the largest layer serves every call.
+ */
+moe_status moe_workspace_bytes(const moe_dims* dims, size_t* bytes);
+
+/*
+ * Router scores and top-k gate (Section II-A).
+ *   logits  [T,E] fp32: written with x . w_router[e] + bias[e] (fp32
+ *           accumulation), or, with MOE_LOGITS_IN, read as given (then x,
+ *           w_router and bias are not used: the scores are final).
+ *   topk_idx [T,k] int32: the k highest scores of each token in decreasing
+ *           order; equal scores go to the lower expert id.
+ *   topk_w  [T,k] fp32: softmax of the k selected scores (renormalised gate);
+ *           a selected score equal to the top one contributes exactly 1, so a
+ *           row of equal scores (also all -inf) gets 1/k.  NaN scores: undefined.
+ */
+moe_status moe_route_topk(const moe_dims* dims, const void* x, const void* w_router, const float* bias,
+                          float* logits, uint32_t flags, int32_t* topk_idx, float* topk_w, void* stream);
+
+/*
+ * Expert-aligned token repacking with the residency split (Section IV-E.1,
+ * Section IV-D.2).
+ *   in:  topk_idx [T,k] (ids outside [0,E) are dropped: no row, inv_perm = -1),
+ *        topk_w [T,k] (read only if off_w != NULL), expert_slot [E],
+ *        x [T,H] (read only if off_rows != NULL)
+ *   out: counts [E]      pairs per expert
+ *        seg_start [E]   first packed row of each expert
+ *        perm [T*k]      pair q stored at packed row p (perm[p] = q)
+ *        inv_perm [T*k]  packed row of pair q
+ *        n_res [1]       resident pairs
+ *        off_rows [T*k, H] (optional): off_rows[p - n_res] = x[perm[p] / k] for
+ *                        the offloaded rows p in [n_res, T*k)
+ *        off_w [T*k] (optional): the matching gate weights
+ * n_res stays in device memory; the caller copies it (and the offloaded list)
+ * to the host when it runs the offloaded experts there.
+ */
+moe_status moe_repack(const moe_dims* dims, const int32_t* topk_idx, const float* topk_w,
+                      const int32_t* expert_slot, const void* x, int32_t* counts, int32_t* seg_start,
+                      int32_t* perm, int32_t* inv_perm, int32_t* n_res, void* off_rows, float* off_w,
+                      void* stream);
+
+/*
+ * Grouped SwiGLU expert FFN over the resident experts and the shared experts
+ * (Section IV-D.2, Section IV-E.1): every resident expert with tokens runs once
+ * over its packed rows; every shared expert runs over all T tokens.
+ *   y [T*k + S*T, H] fp32: row p < T*k is packed row p (written for resident
+ *     rows [0, n_res) only; the offloaded rows are left untouched for the
+ *     host); row T*k + s*T + t is shared expert s on token t.
+ * Counts and offsets are read from device memory: no host synchronisation.
+ * ws13 / ws2 may be NULL when S == 0.
+ */
+moe_status moe_grouped_ffn(const moe_dims* dims, const void* x, const int32_t* perm, const int32_t* counts,
+                           const int32_t* seg_start, const int32_t* expert_slot, const void* w13, const void* w2,
+                           const void* ws13, const void* ws2, float* y, void* ws, size_t ws_bytes, void* stream);
+
+/*
+ * Merge back to token order (Section IV-D.2), deterministic: for each token,
+ * in this fixed order and accumulated in fp32,
+ *   out[t] = sum_j w[t,j] * y[inv_perm[t*k+j]]        (resident experts)
+ *          + sum_j w[t,j] * y_off[inv_perm[t*k+j] - n_res]  (offloaded, only if y_off)
+ *          + sum_s y[T*k + s*T + t]                     (shared experts)
+ * then rounded once to out_dtype (MOE_F32, or MOE_BF16 with round-to-nearest-even).
+ *   y_off [T*k - n_res, H] fp32: the host's outputs for the offloaded list, in
+ *     packed order, or NULL for the resident-plus-shared partial.
+ *   n_res: device pointer, read only if y_off != NULL.
+ */
+moe_status moe_combine(const moe_dims* dims, const int32_t* topk_idx, const float* topk_w,
+                       const int32_t* inv_perm, const int32_t* expert_slot, const float* y,
+                       const float* y_off, const int32_t* n_res, void* out, int32_t out_dtype, void* stream);
+
+/* Arguments of the fused layer forward. */
+typedef struct moe_layer_args {
+    size_t struct_size;          /* sizeof(moe_layer_args) */
+    moe_dims dims;
+    uint32_t flags;              /* MOE_LOGITS_IN */
+    int32_t out_dtype;           /* MOE_F32 or dims.dtype */
+    const void* x;               /* [T,H] (not read with MOE_LOGITS_IN except for shared experts, FFN and off_rows) */
+    const void* w_router;        /* [E,H] (not read with MOE_LOGITS_IN) */
+    const float* bias;           /* [E] or NULL */
+    const int32_t* expert_slot;  /* [E] */
+    const void* w13;             /* [slots, 2F, H] */
+    const void* w2;              /* [slots, H, F] */
+    const void* ws13;            /* [S, 2Fs, H] or NULL if S == 0 */
+    const void* ws2;             /* [S, H, Fs] or NULL if S == 0 */
+    void* out;                   /* [T,H] out_dtype: resident + shared partial output */
+    /* optional outputs; NULL keeps them in the workspace */
+    float* logits;               /* [T,E]; required input with MOE_LOGITS_IN */
+    int32_t* topk_idx;           /* [T,k] */
+    float* topk_w;               /* [T,k] */
+    int32_t* counts;             /* [E] */
+    int32_t* seg_start;          /* [E] */
+    int32_t* perm;               /* [T*k] */
+    int32_t* inv_perm;           /* [T*k] */
+    int32_t* n_res;              /* [1] */
+    void* off_rows;              /* [T*k, H] dims.dtype, packed offloaded rows */
+    float* off_w;                /* [T*k] */
+} moe_layer_args;
+
+/*
+ * Fused forward of one MoE layer: route -> repack (+ offloaded pack) ->
+ * grouped SwiGLU FFN over resident and shared experts -> combine.  `out` holds
+ * the resident-plus-shared output; the offloaded list (off_rows, off_w,
+ * perm[n_res:], n_res) is returned for host execution, whose results the caller
+ * merges with moe_combine(..., y_off, ...).  Needs moe_workspace_bytes(&dims).
+ */
+moe_status moe_layer_forward(const moe_layer_args* args, void* ws, size_t ws_bytes, void* stream);
+
+/*
+ * Stage-aware residency support (Section IV-B.2, Section IV-C.2).
+ * moe_stage_accumulate adds a layer call's per-expert counts into an int64
+ * activation log on the device: log[e] += counts[e].
+ */
+moe_status moe_stage_accumulate(int32_t experts, const int32_t* counts, int64_t* log, void* stream);
+
+/*
+ * Host-side residency plan at a stage boundary (Section IV-C.2): rank the
+ * experts by the completed stage's activation count (ties: lower id first),
+ * keep the top `slots`; an expert that stays keeps its slot, incoming experts
+ * take the freed slots (by rank, freed slots in ascending order).
+ *   log [E] (host), prev_slot [E] (host, -1 = offloaded) -> new_slot [E] (host).
+ * Host memory only; no device work.
+ */
+moe_status moe_stage_plan(int32_t experts, int32_t slots, const int64_t* log, const int32_t* prev_slot,
+                          int32_t* new_slot);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* SAEM_MOE_H */

@@ -165,7 +165,7 @@ def layer_forward(x: np.ndarray, w_router: np.ndarray, bias: Optional[np.ndarray
                   n_shared: int = 0, ws13_of: Optional[Callable[[int], np.ndarray]] = None,
                   ws2_of: Optional[Callable[[int], np.ndarray]] = None,
                   logits: Optional[np.ndarray] = None, idx: Optional[np.ndarray] = None,
-                  sample: Optional[Sequence[int]] = None) -> Dict[str, np.ndarray]:
+                  sample: Optional[Sequence[int]] = None, offloaded: bool = True) -> Dict[str, np.ndarray]:
     """The whole layer, steps 1-5 in the paper's order.
 
     logits: route these scores instead of computing them (fp32 scores are taken
@@ -175,6 +175,7 @@ def layer_forward(x: np.ndarray, w_router: np.ndarray, bias: Optional[np.ndarray
             are still the softmax of the scores over the selection.
     sample: compute outputs only for these tokens (routing and repacking always
             cover the whole batch).
+    offloaded: False skips the offloaded experts (out_off stays zero).
 
     Returns logits, idx, w, counts, seg_start, perm, inv_perm, n_res, and for the
     sampled tokens: out_res (resident routed experts + shared experts),
@@ -201,7 +202,7 @@ def layer_forward(x: np.ndarray, w_router: np.ndarray, bias: Optional[np.ndarray
     res = np.asarray(resident, dtype=bool)
     for e in group_order(res):
         c = int(rp["counts"][e])
-        if c == 0:
+        if c == 0 or (not offloaded and not res[e]):
             continue
         rows = np.arange(rp["seg_start"][e], rp["seg_start"][e] + c)
         pairs = rp["perm"][rows]
@@ -233,12 +234,12 @@ def gate_weights(logits: np.ndarray, idx: np.ndarray) -> np.ndarray:
     return term / term.sum(axis=1, keepdims=True)
 
 
-def layer_forward_synthetic(layer, logits=None, idx=None, sample=None) -> Dict[str, np.ndarray]:
+def layer_forward_synthetic(layer, logits=None, idx=None, sample=None, offloaded=True) -> Dict[str, np.ndarray]:
     """layer_forward on a ``workloads.SyntheticLayer``."""
     c = layer.cfg
     return layer_forward(layer.x, layer.w_router, layer.bias, layer.resident, c.top_k,
                          layer.w13, layer.w2, c.shared, layer.ws13, layer.ws2,
-                         logits=logits, idx=idx, sample=sample)
+                         logits=logits, idx=idx, sample=sample, offloaded=offloaded)
 
 
 def near_tie_alternatives(logits: np.ndarray, k: int, delta: float, max_alternatives: int = 16):

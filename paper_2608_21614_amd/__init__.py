@@ -1,0 +1,178 @@
+"""Python binding of libsaem_moe.so: one MoE layer's forward on MI355X (gfx950).
+
+Argument marshalling only: every function below validates nothing itself
+beyond tensor placement, passes raw device pointers and the current HIP stream
+to the C ABI declared in ``include/saem_moe.h``, and raises ``MoeError`` on a
+non-OK status.  All computation happens in the library's HIP kernels.  There
+is no fallback: importing this package without the built library raises.
+
+Function names are the ABI's.  Shapes and layouts are documented in the header.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+from typing import Optional
+
+HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(HERE, "libsaem_moe.so")
+
+MOE_OK, MOE_ERR_INVALID_ARG, MOE_ERR_UNSUPPORTED, MOE_ERR_WORKSPACE, MOE_ERR_HIP = range(5)
+MOE_F32, MOE_BF16 = 0, 1
+MOE_LOGITS_IN = 1
+
+EXPORTED = [
+    "moe_abi_version", "moe_status_str", "moe_check_dims", "moe_workspace_bytes", "moe_route_topk",
+    "moe_repack", "moe_grouped_ffn", "moe_combine", "moe_layer_forward", "moe_stage_accumulate",
+    "moe_stage_plan",
+]
+
+
+class MoeError(RuntimeError):
+    def __init__(self, status: int, where: str):
+        self.status = status
+        super().__init__(f"{where}: {status_str(status)} (status {status})")
+
+
+class moe_dims(ctypes.Structure):
+    _fields_ = [(n, ctypes.c_int32) for n in
+                ("tokens", "hidden", "experts", "ffn", "top_k", "shared", "shared_ffn", "slots", "dtype")]
+
+
+_vp = ctypes.c_void_p
+
+
+class moe_layer_args(ctypes.Structure):
+    _fields_ = [
+        ("struct_size", ctypes.c_size_t), ("dims", moe_dims), ("flags", ctypes.c_uint32),
+        ("out_dtype", ctypes.c_int32),
+        ("x", _vp), ("w_router", _vp), ("bias", _vp), ("expert_slot", _vp), ("w13", _vp), ("w2", _vp),
+        ("ws13", _vp), ("ws2", _vp), ("out", _vp),
+        ("logits", _vp), ("topk_idx", _vp), ("topk_w", _vp), ("counts", _vp), ("seg_start", _vp),
+        ("perm", _vp), ("inv_perm", _vp), ("n_res", _vp), ("off_rows", _vp), ("off_w", _vp),
+    ]
+
+
+def _load() -> ctypes.CDLL:
+    if not os.path.exists(LIB_PATH):
+        raise ImportError(f"{LIB_PATH} is not built; run `python paper_2608_21614_amd/build.py` "
+                          "(hipcc, gfx950) before using the HIP path")
+    lib = ctypes.CDLL(LIB_PATH)
+    D = ctypes.POINTER(moe_dims)
+    i32, u32, sz = ctypes.c_int32, ctypes.c_uint32, ctypes.c_size_t
+    sig = {
+        "moe_abi_version": ([], ctypes.c_int),
+        "moe_status_str": ([ctypes.c_int], ctypes.c_char_p),
+        "moe_check_dims": ([D], ctypes.c_int),
+        "moe_workspace_bytes": ([D, ctypes.POINTER(ctypes.c_size_t)], ctypes.c_int),
+        "moe_route_topk": ([D, _vp, _vp, _vp, _vp, u32, _vp, _vp, _vp], ctypes.c_int),
+        "moe_repack": ([D, _vp, _vp, _vp, _vp, _vp, _vp, _vp, _vp, _vp, _vp, _vp, _vp], ctypes.c_int),
+        "moe_grouped_ffn": ([D, _vp, _vp, _vp, _vp, _vp, _vp, _vp, _vp, _vp, _vp, _vp, sz, _vp], ctypes.c_int),
+        "moe_combine": ([D, _vp, _vp, _vp, _vp, _vp, _vp, _vp, _vp, i32, _vp], ctypes.c_int),
+        "moe_layer_forward": ([ctypes.POINTER(moe_layer_args), _vp, sz, _vp], ctypes.c_int),
+        "moe_stage_accumulate": ([i32, _vp, _vp, _vp], ctypes.c_int),
+        "moe_stage_plan": ([i32, i32, _vp, _vp, _vp], ctypes.c_int),
+    }
+    for name, (args, res) in sig.items():
+        fn = getattr(lib, name)
+        fn.argtypes = args
+        fn.restype = res
+    return lib
+
+
+lib = _load()
+
+
+def status_str(status: int) -> str:
+    return lib.moe_status_str(int(status)).decode()
+
+
+def _check(status: int, where: str) -> None:
+    if status != MOE_OK:
+        raise MoeError(status, where)
+
+
+def make_dims(tokens: int, hidden: int, experts: int, ffn: int, top_k: int, shared: int = 0, shared_ffn: int = 0,
+              slots: int = 0, dtype: int = MOE_BF16) -> moe_dims:
+    return moe_dims(tokens, hidden, experts, ffn, top_k, shared, shared_ffn, slots, dtype)
+
+
+def _p(t) -> Optional[int]:
+    """Device pointer of a tensor (or None)."""
+    if t is None:
+        return None
+    if t.device.type != "cuda":
+        raise ValueError("libsaem_moe takes device tensors")
+    if not t.is_contiguous():
+        raise ValueError("libsaem_moe takes contiguous tensors")
+    return t.data_ptr()
+
+
+def _stream(stream) -> Optional[int]:
+    import torch
+    s = torch.cuda.current_stream() if stream is None else stream
+    return s.cuda_stream
+
+
+def moe_check_dims(dims: moe_dims) -> int:
+    return lib.moe_check_dims(ctypes.byref(dims))
+
+
+def moe_workspace_bytes(dims: moe_dims) -> int:
+    n = ctypes.c_size_t(0)
+    _check(lib.moe_workspace_bytes(ctypes.byref(dims), ctypes.byref(n)), "moe_workspace_bytes")
+    return int(n.value)
+
+
+def moe_route_topk(dims, x, w_router, bias, logits, topk_idx, topk_w, logits_in: bool = False, stream=None):
+    _check(lib.moe_route_topk(ctypes.byref(dims), _p(x), _p(w_router), _p(bias), _p(logits),
+                              MOE_LOGITS_IN if logits_in else 0, _p(topk_idx), _p(topk_w), _stream(stream)),
+           "moe_route_topk")
+
+
+def moe_repack(dims, topk_idx, topk_w, expert_slot, x, counts, seg_start, perm, inv_perm, n_res,
+               off_rows=None, off_w=None, stream=None):
+    _check(lib.moe_repack(ctypes.byref(dims), _p(topk_idx), _p(topk_w), _p(expert_slot), _p(x), _p(counts),
+                          _p(seg_start), _p(perm), _p(inv_perm), _p(n_res), _p(off_rows), _p(off_w),
+                          _stream(stream)), "moe_repack")
+
+
+def moe_grouped_ffn(dims, x, perm, counts, seg_start, expert_slot, w13, w2, ws13, ws2, y, ws, stream=None):
+    _check(lib.moe_grouped_ffn(ctypes.byref(dims), _p(x), _p(perm), _p(counts), _p(seg_start), _p(expert_slot),
+                               _p(w13), _p(w2), _p(ws13), _p(ws2), _p(y), _p(ws), ws.numel() * ws.element_size(),
+                               _stream(stream)), "moe_grouped_ffn")
+
+
+def moe_combine(dims, topk_idx, topk_w, inv_perm, expert_slot, y, y_off, n_res, out, out_dtype: int, stream=None):
+    _check(lib.moe_combine(ctypes.byref(dims), _p(topk_idx), _p(topk_w), _p(inv_perm), _p(expert_slot), _p(y),
+                           _p(y_off), _p(n_res), _p(out), int(out_dtype), _stream(stream)), "moe_combine")
+
+
+def layer_args(dims, x, w_router, bias, expert_slot, w13, w2, ws13, ws2, out, out_dtype: int, flags: int = 0,
+               logits=None, topk_idx=None, topk_w=None, counts=None, seg_start=None, perm=None, inv_perm=None,
+               n_res=None, off_rows=None, off_w=None) -> moe_layer_args:
+    """Fills a moe_layer_args struct (kept alive by the caller while launches use it)."""
+    return moe_layer_args(
+        ctypes.sizeof(moe_layer_args), dims, flags, out_dtype, _p(x), _p(w_router), _p(bias), _p(expert_slot),
+        _p(w13), _p(w2), _p(ws13), _p(ws2), _p(out), _p(logits), _p(topk_idx), _p(topk_w), _p(counts),
+        _p(seg_start), _p(perm), _p(inv_perm), _p(n_res), _p(off_rows), _p(off_w))
+
+
+def moe_layer_forward(args: moe_layer_args, ws, stream=None):
+    _check(lib.moe_layer_forward(ctypes.byref(args), _p(ws), ws.numel() * ws.element_size(), _stream(stream)),
+           "moe_layer_forward")
+
+
+def moe_stage_accumulate(experts: int, counts, log, stream=None):
+    _check(lib.moe_stage_accumulate(int(experts), _p(counts), _p(log), _stream(stream)), "moe_stage_accumulate")
+
+
+def moe_stage_plan(log_host, prev_slot_host, slots: int):
+    """Host-side residency plan (numpy int64 log, int32 prev slots) -> numpy int32 new slots."""
+    import numpy as np
+    log = np.ascontiguousarray(log_host, dtype=np.int64)
+    prev = np.ascontiguousarray(prev_slot_host, dtype=np.int32)
+    new = np.empty_like(prev)
+    _check(lib.moe_stage_plan(int(log.size), int(slots), log.ctypes.data, prev.ctypes.data, new.ctypes.data),
+           "moe_stage_plan")
+    return new

@@ -1,0 +1,287 @@
+// abi.hip -- the C ABI of libsaem_moe.so: host-side validation, workspace
+// layout and launch sequencing.  Every check runs on the host before anything
+// is enqueued and never touches device memory.
+#include <string.h>
+
+#include <algorithm>
+
+#include "../../include/saem_moe.h"
+#include "kernels.hpp"
+
+namespace {
+
+using saem::Shape;
+
+constexpr long long kMaxRows = 1ll << 24;  // T*k + S*T rows handled by one call
+
+bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
+bool ok_ptr(const void* p) { return p != nullptr && aligned16(p); }
+bool ok_opt(const void* p) { return p == nullptr || aligned16(p); }
+// A required array: non-NULL and aligned, except that an array with no elements may be NULL.
+bool ok_arr(const void* p, long long n) { return n == 0 ? aligned16(p) : ok_ptr(p); }
+
+moe_status check_dims(const moe_dims* d) {
+    if (!d) return MOE_ERR_INVALID_ARG;
+    if (d->tokens < 0 || d->hidden <= 0 || d->experts <= 0 || d->ffn <= 0 || d->top_k <= 0 || d->shared < 0 ||
+        d->slots < 0)
+        return MOE_ERR_INVALID_ARG;
+    if (d->dtype != MOE_F32 && d->dtype != MOE_BF16) return MOE_ERR_INVALID_ARG;
+    if (d->top_k > d->experts || d->slots > d->experts) return MOE_ERR_INVALID_ARG;
+    if (d->shared > 0 && d->shared_ffn <= 0) return MOE_ERR_INVALID_ARG;
+    if (d->experts > 256 || d->top_k > 8 || d->shared > 8) return MOE_ERR_UNSUPPORTED;
+    if (d->hidden % 64 != 0 || d->ffn % 64 != 0) return MOE_ERR_UNSUPPORTED;
+    if (d->shared > 0 && d->shared_ffn % 64 != 0) return MOE_ERR_UNSUPPORTED;
+    const long long rows = (long long)d->tokens * d->top_k + (long long)d->shared * d->tokens;
+    if (rows > kMaxRows) return MOE_ERR_UNSUPPORTED;
+    if ((long long)d->hidden > (1 << 20) || (long long)d->ffn > (1 << 20) || (long long)d->shared_ffn > (1 << 20))
+        return MOE_ERR_UNSUPPORTED;
+    return MOE_OK;
+}
+
+Shape shape_of(const moe_dims* d) {
+    Shape s;
+    s.T = d->tokens;
+    s.H = d->hidden;
+    s.E = d->experts;
+    s.F = d->ffn;
+    s.k = d->top_k;
+    s.S = d->shared;
+    s.Fs = d->shared > 0 ? d->shared_ffn : 0;
+    s.slots = d->slots;
+    s.bf16 = d->dtype == MOE_BF16 ? 1 : 0;
+    return s;
+}
+
+// Workspace layout (256-byte aligned regions).
+struct Layout {
+    size_t logits, idx, w, counts, seg, nres, perm, inv, act, y, total;
+    int ks, Fa;
+    long long rows;
+};
+
+size_t align256(size_t v) { return (v + 255) & ~size_t(255); }
+
+Layout layout_of(const Shape& s) {
+    Layout L;
+    const size_t T = s.T, E = s.E, k = s.k, H = s.H;
+    L.rows = (long long)s.T * s.k + (long long)s.S * s.T;
+    L.Fa = std::max(s.F, s.Fs);
+    L.ks = saem::ffn_down_splits(s);
+    size_t off = 0;
+    auto take = [&](size_t bytes) {
+        const size_t at = off;
+        off = align256(off + std::max<size_t>(bytes, 1));
+        return at;
+    };
+    L.logits = take(T * E * 4);
+    L.idx = take(T * k * 4);
+    L.w = take(T * k * 4);
+    L.counts = take(E * 4);
+    L.seg = take(E * 4);
+    L.nres = take(4);
+    L.perm = take(T * k * 4);
+    L.inv = take(T * k * 4);
+    L.act = take((size_t)L.rows * L.Fa * (s.bf16 ? 2 : 4));
+    L.y = take((size_t)L.ks * L.rows * H * 4);
+    L.total = off;
+    return L;
+}
+
+template <typename T>
+T* at(void* ws, size_t off) {
+    return reinterpret_cast<T*>(static_cast<char*>(ws) + off);
+}
+
+moe_status hip_status(hipError_t e) { return e == hipSuccess ? MOE_OK : MOE_ERR_HIP; }
+
+}  // namespace
+
+extern "C" {
+
+int moe_abi_version(void) { return MOE_ABI_VERSION; }
+
+const char* moe_status_str(moe_status s) {
+    switch (s) {
+        case MOE_OK: return "ok";
+        case MOE_ERR_INVALID_ARG: return "invalid argument";
+        case MOE_ERR_UNSUPPORTED: return "unsupported shape or option";
+        case MOE_ERR_WORKSPACE: return "workspace missing or too small";
+        case MOE_ERR_HIP: return "HIP launch or runtime error";
+    }
+    return "unknown status";
+}
+
+moe_status moe_check_dims(const moe_dims* dims) { return check_dims(dims); }
+
+moe_status moe_workspace_bytes(const moe_dims* dims, size_t* bytes) {
+    const moe_status st = check_dims(dims);
+    if (st != MOE_OK) return st;
+    if (!bytes) return MOE_ERR_INVALID_ARG;
+    *bytes = layout_of(shape_of(dims)).total;
+    return MOE_OK;
+}
+
+moe_status moe_route_topk(const moe_dims* dims, const void* x, const void* w_router, const float* bias,
+                          float* logits, uint32_t flags, int32_t* topk_idx, float* topk_w, void* stream) {
+    moe_status st = check_dims(dims);
+    if (st != MOE_OK) return st;
+    if (flags & ~MOE_LOGITS_IN) return MOE_ERR_INVALID_ARG;
+    const bool lin = (flags & MOE_LOGITS_IN) != 0;
+    const long long T = dims->tokens;
+    if (!ok_arr(logits, T) || !ok_arr(topk_idx, T) || !ok_arr(topk_w, T)) return MOE_ERR_INVALID_ARG;
+    if (!lin && (!ok_arr(x, T) || !ok_ptr(w_router) || !ok_opt(bias))) return MOE_ERR_INVALID_ARG;
+    const Shape s = shape_of(dims);
+    return hip_status(saem::launch_route_topk(s, x, w_router, lin ? nullptr : bias, logits, lin, topk_idx, topk_w,
+                                              static_cast<hipStream_t>(stream)));
+}
+
+moe_status moe_repack(const moe_dims* dims, const int32_t* topk_idx, const float* topk_w,
+                      const int32_t* expert_slot, const void* x, int32_t* counts, int32_t* seg_start,
+                      int32_t* perm, int32_t* inv_perm, int32_t* n_res, void* off_rows, float* off_w,
+                      void* stream) {
+    moe_status st = check_dims(dims);
+    if (st != MOE_OK) return st;
+    const long long T = dims->tokens;
+    if (!ok_arr(topk_idx, T) || !ok_ptr(expert_slot) || !ok_ptr(counts) || !ok_ptr(seg_start) || !ok_arr(perm, T) ||
+        !ok_arr(inv_perm, T) || !ok_ptr(n_res) || !ok_opt(off_rows) || !ok_opt(off_w))
+        return MOE_ERR_INVALID_ARG;
+    if (off_rows && !ok_arr(x, T)) return MOE_ERR_INVALID_ARG;
+    if (off_w && !ok_arr(topk_w, T)) return MOE_ERR_INVALID_ARG;
+    const Shape s = shape_of(dims);
+    hipStream_t hs = static_cast<hipStream_t>(stream);
+    hipError_t e = saem::launch_repack(s, topk_idx, expert_slot, counts, seg_start, perm, inv_perm, n_res, hs);
+    if (e == hipSuccess) e = saem::launch_offload_pack(s, x, topk_w, perm, n_res, off_rows, off_w, hs);
+    return hip_status(e);
+}
+
+moe_status moe_grouped_ffn(const moe_dims* dims, const void* x, const int32_t* perm, const int32_t* counts,
+                           const int32_t* seg_start, const int32_t* expert_slot, const void* w13, const void* w2,
+                           const void* ws13, const void* ws2, float* y, void* ws, size_t ws_bytes, void* stream) {
+    moe_status st = check_dims(dims);
+    if (st != MOE_OK) return st;
+    const long long T = dims->tokens;
+    if (!ok_arr(x, T) || !ok_arr(perm, T) || !ok_ptr(counts) || !ok_ptr(seg_start) || !ok_ptr(expert_slot) ||
+        !ok_arr(y, T))
+        return MOE_ERR_INVALID_ARG;
+    if (dims->slots > 0 && (!ok_ptr(w13) || !ok_ptr(w2))) return MOE_ERR_INVALID_ARG;
+    if (dims->shared > 0 && (!ok_ptr(ws13) || !ok_ptr(ws2))) return MOE_ERR_INVALID_ARG;
+    const Shape s = shape_of(dims);
+    const Layout L = layout_of(s);
+    if (!ws || ws_bytes < L.total || !aligned16(ws)) return MOE_ERR_WORKSPACE;
+    hipStream_t hs = static_cast<hipStream_t>(stream);
+    saem::FfnArgs a;
+    a.x = x; a.perm = perm; a.counts = counts; a.seg_start = seg_start; a.expert_slot = expert_slot;
+    a.w13 = w13; a.w2 = w2; a.ws13 = ws13; a.ws2 = ws2;
+    a.act = at<char>(ws, L.act);
+    a.Fa = L.Fa;
+    a.ks = L.ks;
+    a.y_ks_stride = L.rows * (long long)s.H;
+    a.y = (L.ks == 1) ? y : at<float>(ws, L.y);
+    hipError_t e = saem::launch_grouped_ffn(s, a, hs);
+    if (e == hipSuccess && L.ks > 1)
+        e = saem::launch_reduce_splits(s, counts, expert_slot, a.y, L.ks, a.y_ks_stride, y, hs);
+    return hip_status(e);
+}
+
+moe_status moe_combine(const moe_dims* dims, const int32_t* topk_idx, const float* topk_w,
+                       const int32_t* inv_perm, const int32_t* expert_slot, const float* y,
+                       const float* y_off, const int32_t* n_res, void* out, int32_t out_dtype, void* stream) {
+    moe_status st = check_dims(dims);
+    if (st != MOE_OK) return st;
+    if (out_dtype != MOE_F32 && out_dtype != MOE_BF16) return MOE_ERR_INVALID_ARG;
+    const long long T = dims->tokens;
+    if (!ok_arr(topk_idx, T) || !ok_arr(topk_w, T) || !ok_arr(inv_perm, T) || !ok_ptr(expert_slot) ||
+        !ok_arr(y, T) || !ok_arr(out, T) || !ok_opt(y_off))
+        return MOE_ERR_INVALID_ARG;
+    if (y_off && !ok_ptr(n_res)) return MOE_ERR_INVALID_ARG;
+    const Shape s = shape_of(dims);
+    return hip_status(saem::launch_combine(s, topk_idx, topk_w, inv_perm, expert_slot, y, 1, 0, y_off, n_res, out,
+                                           out_dtype == MOE_BF16, static_cast<hipStream_t>(stream)));
+}
+
+moe_status moe_layer_forward(const moe_layer_args* a, void* ws, size_t ws_bytes, void* stream) {
+    if (!a || a->struct_size != sizeof(moe_layer_args)) return MOE_ERR_INVALID_ARG;
+    const moe_dims* d = &a->dims;
+    moe_status st = check_dims(d);
+    if (st != MOE_OK) return st;
+    if (a->flags & ~MOE_LOGITS_IN) return MOE_ERR_INVALID_ARG;
+    if (a->out_dtype != MOE_F32 && a->out_dtype != MOE_BF16) return MOE_ERR_INVALID_ARG;
+    const bool lin = (a->flags & MOE_LOGITS_IN) != 0;
+    const long long T = d->tokens;
+    if (!ok_arr(a->x, T) || !ok_ptr(a->expert_slot) || !ok_arr(a->out, T)) return MOE_ERR_INVALID_ARG;
+    if (!lin && (!ok_ptr(a->w_router) || !ok_opt(a->bias))) return MOE_ERR_INVALID_ARG;
+    if (lin && !ok_arr(a->logits, T)) return MOE_ERR_INVALID_ARG;
+    if (d->slots > 0 && (!ok_ptr(a->w13) || !ok_ptr(a->w2))) return MOE_ERR_INVALID_ARG;
+    if (d->shared > 0 && (!ok_ptr(a->ws13) || !ok_ptr(a->ws2))) return MOE_ERR_INVALID_ARG;
+    if (!ok_opt(a->logits) || !ok_opt(a->topk_idx) || !ok_opt(a->topk_w) || !ok_opt(a->counts) ||
+        !ok_opt(a->seg_start) || !ok_opt(a->perm) || !ok_opt(a->inv_perm) || !ok_opt(a->n_res) ||
+        !ok_opt(a->off_rows) || !ok_opt(a->off_w))
+        return MOE_ERR_INVALID_ARG;
+    const Shape s = shape_of(d);
+    const Layout L = layout_of(s);
+    if (!ws || ws_bytes < L.total || !aligned16(ws)) return MOE_ERR_WORKSPACE;
+    hipStream_t hs = static_cast<hipStream_t>(stream);
+
+    float* logits = a->logits ? a->logits : at<float>(ws, L.logits);
+    int32_t* idx = a->topk_idx ? a->topk_idx : at<int32_t>(ws, L.idx);
+    float* w = a->topk_w ? a->topk_w : at<float>(ws, L.w);
+    int32_t* counts = a->counts ? a->counts : at<int32_t>(ws, L.counts);
+    int32_t* seg = a->seg_start ? a->seg_start : at<int32_t>(ws, L.seg);
+    int32_t* perm = a->perm ? a->perm : at<int32_t>(ws, L.perm);
+    int32_t* inv = a->inv_perm ? a->inv_perm : at<int32_t>(ws, L.inv);
+    int32_t* nres = a->n_res ? a->n_res : at<int32_t>(ws, L.nres);
+
+    hipError_t e = saem::launch_route_topk(s, a->x, a->w_router, lin ? nullptr : a->bias, logits, lin, idx, w, hs);
+    if (e == hipSuccess) e = saem::launch_repack(s, idx, a->expert_slot, counts, seg, perm, inv, nres, hs);
+    if (s.T == 0) return hip_status(e);
+    if (e == hipSuccess) e = saem::launch_offload_pack(s, a->x, w, perm, nres, a->off_rows, a->off_w, hs);
+    saem::FfnArgs f;
+    f.x = a->x; f.perm = perm; f.counts = counts; f.seg_start = seg; f.expert_slot = a->expert_slot;
+    f.w13 = a->w13; f.w2 = a->w2; f.ws13 = a->ws13; f.ws2 = a->ws2;
+    f.act = at<char>(ws, L.act);
+    f.Fa = L.Fa;
+    f.y = at<float>(ws, L.y);
+    f.ks = L.ks;
+    f.y_ks_stride = L.rows * (long long)s.H;
+    if (e == hipSuccess) e = saem::launch_grouped_ffn(s, f, hs);
+    if (e == hipSuccess)
+        e = saem::launch_combine(s, idx, w, inv, a->expert_slot, f.y, L.ks, f.y_ks_stride, nullptr, nullptr, a->out,
+                                 a->out_dtype == MOE_BF16, hs);
+    return hip_status(e);
+}
+
+moe_status moe_stage_accumulate(int32_t experts, const int32_t* counts, int64_t* log, void* stream) {
+    if (experts <= 0 || experts > 256 || !ok_ptr(counts) || !ok_ptr(log)) return MOE_ERR_INVALID_ARG;
+    return hip_status(saem::launch_stage_accumulate(experts, counts, log, static_cast<hipStream_t>(stream)));
+}
+
+moe_status moe_stage_plan(int32_t experts, int32_t slots, const int64_t* log, const int32_t* prev_slot,
+                          int32_t* new_slot) {
+    if (experts <= 0 || experts > 256 || slots < 0 || slots > experts || !log || !prev_slot || !new_slot)
+        return MOE_ERR_INVALID_ARG;
+    int order[256];
+    for (int e = 0; e < experts; ++e) order[e] = e;
+    std::stable_sort(order, order + experts, [&](int a, int b) { return log[a] > log[b]; });
+    bool keep[256] = {false};
+    for (int i = 0; i < slots; ++i) keep[order[i]] = true;
+    bool used[256] = {false};
+    for (int e = 0; e < experts; ++e) {
+        new_slot[e] = -1;
+        const int ps = prev_slot[e];
+        if (keep[e] && ps >= 0 && ps < slots && !used[ps]) {
+            new_slot[e] = ps;
+            used[ps] = true;
+        }
+    }
+    int next_free = 0;
+    for (int i = 0; i < slots; ++i) {
+        const int e = order[i];
+        if (new_slot[e] >= 0) continue;
+        while (next_free < slots && used[next_free]) ++next_free;
+        new_slot[e] = next_free;
+        used[next_free] = true;
+    }
+    return MOE_OK;
+}
+
+}  // extern "C"

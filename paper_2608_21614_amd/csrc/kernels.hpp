@@ -1,0 +1,61 @@
+// kernels.hpp -- internal launch interface between the C ABI (abi.hip) and the kernels.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stddef.h>
+#include <stdint.h>
+
+namespace saem {
+
+// Shapes of one layer, already validated by the ABI.
+struct Shape {
+    int T, H, E, F, k, S, Fs, slots;
+    int bf16;  // 1: bf16 activations and weights, 0: fp32
+};
+
+// Router scores + top-k gate.
+hipError_t launch_route_topk(const Shape& s, const void* x, const void* w_router, const float* bias, float* logits,
+                             bool logits_in, int32_t* topk_idx, float* topk_w, hipStream_t st);
+
+// Histogram, group-order scan, stable permutation, residency split.
+hipError_t launch_repack(const Shape& s, const int32_t* topk_idx, const int32_t* expert_slot, int32_t* counts,
+                         int32_t* seg_start, int32_t* perm, int32_t* inv_perm, int32_t* n_res, hipStream_t st);
+
+// Packs the rows of the offloaded pairs: off_rows[p - n_res] = x[perm[p] / k], off_w[p - n_res] = w[perm[p]].
+hipError_t launch_offload_pack(const Shape& s, const void* x, const float* topk_w, const int32_t* perm,
+                               const int32_t* n_res, void* off_rows, float* off_w, hipStream_t st);
+
+// Grouped SwiGLU FFN.  Row space: packed rows [0, T*k) then shared rows T*k + s*T + t.
+struct FfnArgs {
+    const void* x;
+    const int32_t* perm;
+    const int32_t* counts;
+    const int32_t* seg_start;
+    const int32_t* expert_slot;
+    const void* w13;
+    const void* w2;
+    const void* ws13;
+    const void* ws2;
+    void* act;          // [rows, Fa] activation dtype: silu(x W1) * (x W3)
+    int Fa;             // row stride of act = max(F, Fs)
+    float* y;           // [ks][rows][H] fp32 partial sums over K chunks of the down projection
+    int ks;             // number of K chunks of the down projection
+    long long y_ks_stride;
+};
+
+// Number of K chunks the down projection is split into (1 = direct sums).
+int ffn_down_splits(const Shape& s);
+hipError_t launch_grouped_ffn(const Shape& s, const FfnArgs& a, hipStream_t st);
+
+// y_out[p] = sum_c y[c][p] for the resident packed rows and the shared rows.
+hipError_t launch_reduce_splits(const Shape& s, const int32_t* counts, const int32_t* expert_slot, const float* y,
+                                int ks, long long y_ks_stride, float* y_out, hipStream_t st);
+
+// Deterministic combine back to token order.
+hipError_t launch_combine(const Shape& s, const int32_t* topk_idx, const float* topk_w, const int32_t* inv_perm,
+                          const int32_t* expert_slot, const float* y, int ks, long long y_ks_stride,
+                          const float* y_off, const int32_t* n_res, void* out, bool out_bf16, hipStream_t st);
+
+hipError_t launch_stage_accumulate(int E, const int32_t* counts, int64_t* log, hipStream_t st);
+
+}  // namespace saem

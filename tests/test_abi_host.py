@@ -1,0 +1,174 @@
+"""C-ABI host-side behaviour (no GPU): the library loads, exports every symbol the
+header declares, validates arguments on the host, and its host-only stage plan
+matches the oracle's."""
+import ctypes
+import os
+import re
+
+import numpy as np
+import pytest
+
+import oracle
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "saem_moe.h")
+
+
+@pytest.fixture(scope="module")
+def pkg():
+    import paper_2608_21614_amd as p
+    return p
+
+
+def declared_functions():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(moe_[a-z_]+)\s*\(", text)))
+
+
+def test_header_declarations_are_exported(pkg):
+    names = declared_functions()
+    assert len(names) >= 11
+    lib = ctypes.CDLL(pkg.LIB_PATH)
+    for n in names:
+        assert hasattr(lib, n), f"{n} declared in saem_moe.h but not exported"
+    assert sorted(pkg.EXPORTED) == names
+
+
+def test_struct_layout_matches_header(pkg, tmp_path):
+    """The ctypes mirrors have the C compiler's size and field offsets for both structs."""
+    fields = {"moe_dims": [f for f, _ in pkg.moe_dims._fields_],
+              "moe_layer_args": [f for f, _ in pkg.moe_layer_args._fields_]}
+    lines = ['#include <stdio.h>', '#include <stddef.h>', f'#include "{HEADER}"', "int main(void) {"]
+    for st, fs in fields.items():
+        lines.append(f'printf("{st} %zu\\n", sizeof({st}));')
+        for f in fs:
+            lines.append(f'printf("{st}.{f} %zu\\n", offsetof({st}, {f}));')
+    lines.append("return 0; }")
+    src = tmp_path / "layout.c"
+    src.write_text("\n".join(lines))
+    exe = tmp_path / "layout"
+    import subprocess
+    subprocess.run(["gcc", "-std=c11", "-o", str(exe), str(src)], check=True)
+    out = dict(l.rsplit(" ", 1) for l in subprocess.run([str(exe)], capture_output=True, text=True,
+                                                        check=True).stdout.split("\n") if l)
+    for st, cls in (("moe_dims", pkg.moe_dims), ("moe_layer_args", pkg.moe_layer_args)):
+        assert int(out[st]) == ctypes.sizeof(cls)
+        for f in fields[st]:
+            assert int(out[f"{st}.{f}"]) == getattr(cls, f).offset, f"{st}.{f}"
+
+
+def test_version_and_status_strings(pkg):
+    assert pkg.lib.moe_abi_version() == 1
+    assert pkg.status_str(0) == "ok"
+    for s in range(1, 5):
+        assert pkg.status_str(s) and pkg.status_str(s) != "ok"
+
+
+GOOD = dict(tokens=32, hidden=4096, experts=8, ffn=14336, top_k=2, shared=0, shared_ffn=0, slots=4, dtype=1)
+
+
+@pytest.mark.parametrize("field,value,expect", [
+    ("tokens", -1, 1), ("hidden", 0, 1), ("experts", 0, 1), ("ffn", -64, 1), ("top_k", 0, 1), ("top_k", 9, 1),
+    ("slots", -1, 1), ("slots", 9, 1), ("dtype", 7, 1), ("shared", -1, 1),
+    ("experts", 300, 2), ("hidden", 4100, 2), ("ffn", 1400, 2),
+])
+def test_check_dims_rejects(pkg, field, value, expect):
+    d = dict(GOOD, **{field: value})
+    if field == "experts" and value == 300:
+        d["top_k"] = 2
+    assert pkg.moe_check_dims(pkg.make_dims(**d)) == expect
+
+
+def test_check_dims_limits(pkg):
+    assert pkg.moe_check_dims(pkg.make_dims(**GOOD)) == 0
+    assert pkg.moe_check_dims(pkg.make_dims(**dict(GOOD, experts=256, top_k=8, slots=256))) == 0
+    assert pkg.moe_check_dims(pkg.make_dims(**dict(GOOD, experts=16, top_k=9, slots=4))) == 2  # k > 8
+    assert pkg.moe_check_dims(pkg.make_dims(**dict(GOOD, shared=1, shared_ffn=0))) == 1
+    assert pkg.moe_check_dims(pkg.make_dims(**dict(GOOD, shared=1, shared_ffn=100))) == 2
+    assert pkg.moe_check_dims(pkg.make_dims(**dict(GOOD, tokens=0))) == 0
+    assert pkg.lib.moe_check_dims(None) == 1
+
+
+def test_workspace_bytes(pkg):
+    n = pkg.moe_workspace_bytes(pkg.make_dims(**GOOD))
+    # at least: activations A (64 rows x F bf16) and fp32 expert outputs (64 rows x H)
+    assert n >= 64 * 14336 * 2 + 64 * 4096 * 4
+    n0 = pkg.moe_workspace_bytes(pkg.make_dims(**dict(GOOD, tokens=0)))
+    assert 0 < n0 < n
+    big = pkg.moe_workspace_bytes(pkg.make_dims(tokens=2048, hidden=2048, experts=64, ffn=1408, top_k=6, shared=2,
+                                                shared_ffn=1408, slots=48, dtype=1))
+    assert big >= (2048 * 6 + 2 * 2048) * 2048 * 4
+    with pytest.raises(pkg.MoeError):
+        pkg.moe_workspace_bytes(pkg.make_dims(**dict(GOOD, top_k=0)))
+
+
+def _fake(addr=0x10000):
+    return ctypes.c_void_p(addr)
+
+
+def test_invalid_pointers_rejected_before_any_launch(pkg):
+    """NULL or misaligned pointers return MOE_ERR_INVALID_ARG (nothing is enqueued, no device touched)."""
+    lib = pkg.lib
+    d = ctypes.byref(pkg.make_dims(**GOOD))
+    f = _fake()
+    # route: NULL outputs
+    assert lib.moe_route_topk(d, f, f, None, None, 0, f, f, None) == 1
+    # route: misaligned x
+    assert lib.moe_route_topk(d, _fake(0x10004), f, None, f, 0, f, f, None) == 1
+    # route: unknown flag
+    assert lib.moe_route_topk(d, f, f, None, f, 4, f, f, None) == 1
+    # repack: off_rows requested without x
+    assert lib.moe_repack(d, f, f, f, None, f, f, f, f, f, f, None, None) == 1
+    # combine: bad out dtype, y_off without n_res
+    assert lib.moe_combine(d, f, f, f, f, f, None, None, f, 5, None) == 1
+    assert lib.moe_combine(d, f, f, f, f, f, f, None, f, 1, None) == 1
+    # grouped ffn: workspace too small
+    assert lib.moe_grouped_ffn(d, f, f, f, f, f, f, f, None, None, f, f, 16, None) == 3
+    assert lib.moe_grouped_ffn(d, f, f, f, f, f, f, f, None, None, f, None, 1 << 40, None) == 3
+    # shared experts declared but no shared weights
+    d2 = ctypes.byref(pkg.make_dims(**dict(GOOD, shared=1, shared_ffn=128)))
+    assert lib.moe_grouped_ffn(d2, f, f, f, f, f, f, f, None, None, f, f, 1 << 40, None) == 1
+    # stage accumulate
+    assert lib.moe_stage_accumulate(0, f, f, None) == 1
+    assert lib.moe_stage_accumulate(8, None, f, None) == 1
+
+
+def test_layer_forward_struct_checks(pkg):
+    lib = pkg.lib
+    args = pkg.moe_layer_args()
+    args.struct_size = ctypes.sizeof(pkg.moe_layer_args)
+    args.dims = pkg.make_dims(**GOOD)
+    f = 0x10000
+    args.x = args.w_router = args.expert_slot = args.w13 = args.w2 = args.out = f
+    args.out_dtype = 1
+    assert lib.moe_layer_forward(ctypes.byref(args), _fake(), 16, None) == 3          # workspace too small
+    args.struct_size = 8
+    assert lib.moe_layer_forward(ctypes.byref(args), _fake(), 1 << 40, None) == 1     # wrong struct size
+    args.struct_size = ctypes.sizeof(pkg.moe_layer_args)
+    args.flags = 1                                                                     # logits in, no logits
+    assert lib.moe_layer_forward(ctypes.byref(args), _fake(), 1 << 40, None) == 1
+    args.flags = 0
+    args.out_dtype = 3
+    assert lib.moe_layer_forward(ctypes.byref(args), _fake(), 1 << 40, None) == 1
+    assert lib.moe_layer_forward(None, _fake(), 1 << 40, None) == 1
+
+
+@pytest.mark.parametrize("seed", range(40))
+def test_stage_plan_matches_oracle(pkg, seed):
+    rng = np.random.default_rng(seed)
+    E = int(rng.integers(1, 40))
+    slots = int(rng.integers(0, E + 1))
+    log = rng.integers(0, 6, size=E).astype(np.int64)  # small values: many ties
+    prev = np.full(E, -1, dtype=np.int32)
+    inc = rng.choice(E, slots, replace=False)
+    prev[inc] = rng.permutation(slots)
+    got = pkg.moe_stage_plan(log, prev, slots)
+    want = oracle.stage_plan(log, slots, prev)
+    np.testing.assert_array_equal(got, want)
+    assert sorted(got[got >= 0].tolist()) == list(range(slots))
+
+
+def test_stage_plan_rejects_bad_args(pkg):
+    with pytest.raises(pkg.MoeError):
+        pkg.moe_stage_plan(np.zeros(4, np.int64), np.full(4, -1, np.int32), 5)
