@@ -1,0 +1,244 @@
+#!/usr/bin/env python
+"""MoE-layer forward throughput on one MI355X.
+
+One step = one fused ``moe_layer_forward`` call on one decode batch: router
+scores + top-k gate, expert-aligned repacking with the residency split, the
+pack of the offloaded rows, the grouped SwiGLU FFN over the resident experts
+(two kernels), and the deterministic combine.  The inputs are resident in HBM
+before timing starts; each step uses the next of ``--copies`` copies of the
+expert weights so that no step finds the previous step's weights in the
+256 MB last-level cache.
+
+Prints one JSON line on stdout:
+* value: tokens per second of the whole layer forward;
+* roofline: the dominant kernel (FFN phase 1: gate/up projections + SwiGLU),
+  its algorithmic bytes per launch / its mean duration from HIP events recorded
+  by the library around that kernel on the launch stream, against 8 TB/s;
+* cpu_baseline: the CPU oracle timed on this host on the same workload.
+"""
+from __future__ import annotations
+
+import argparse
+import ctypes
+import hashlib
+import json
+import os
+import re
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+HBM_PEAK_GBPS = 8000.0          # MI355X HBM3E, 8 TB/s
+MFMA_BF16_PEAK_TFLOPS = 2500.0  # dense bf16
+METRIC = "MoE-layer tokens/sec + achieved HBM GB/s (expert weights) at decode batch"
+DOMINANT = "ffn_phase1"         # stage name of the dominant kernel
+TRAFFIC_FILE = os.path.join(ROOT, "profiles", "traffic_ffn_phase1_c2_mixtral_decode.txt")
+KERNEL_SOURCES = [os.path.join(ROOT, "paper_2608_21614_amd", "csrc", n) for n in ("ffn.hip", "common.hpp")]
+STAGES = ["route_topk", "repack", "offload_pack", "ffn_phase1", "ffn_phase2", "combine"]
+
+
+def log(*a):
+    print(*a, file=sys.stderr, flush=True)
+
+
+def kernel_source_hash() -> str:
+    h = hashlib.sha256()
+    for p in KERNEL_SOURCES:
+        with open(p, "rb") as f:
+            h.update(f.read())
+    return h.hexdigest()[:16]
+
+
+def read_traffic(workload: str):
+    """HBM bytes per launch of the dominant kernel from committed counter runs, or None if stale/missing."""
+    if not os.path.exists(TRAFFIC_FILE):
+        return None
+    kv = {}
+    for line in open(TRAFFIC_FILE):
+        m = re.match(r"^([a-z_]+):\s*(\S+)", line.strip())
+        if m:
+            kv[m.group(1)] = m.group(2)
+    if kv.get("source_sha") != kernel_source_hash() or kv.get("workload") != workload:
+        return None
+    try:
+        return float(kv["traffic_bytes_per_launch"])
+    except (KeyError, ValueError):
+        return None
+
+
+def algorithmic_bytes(cfg, counts, resident):
+    """Bytes the method must move, per SwiGLU expert 3*H*F*b, only activated resident experts count."""
+    b = 2 if cfg.dtype == "bf16" else 4
+    T, H, E, F, k = cfg.tokens, cfg.hidden, cfg.experts, cfg.ffn, cfg.top_k
+    active = [e for e in range(E) if resident[e] and counts[e] > 0]
+    n_res = int(sum(counts[e] for e in range(E) if resident[e]))
+    n_off = T * k - n_res
+    w_expert_p1 = 2 * H * F * b * len(active) + cfg.shared * 2 * H * cfg.shared_ffn * b
+    w_expert_all = 3 * H * F * b * len(active) + cfg.shared * 3 * H * cfg.shared_ffn * b
+    phase1 = w_expert_p1 + T * H * b                 # W1,W3 of activated experts + the tokens
+    layer = w_expert_all + H * E * b + T * H * b + T * H * b + n_off * H * b + T * k * 16
+    flops = 6 * H * F * n_res + cfg.shared * 6 * H * cfg.shared_ffn * T + 2 * T * H * E
+    return dict(active=len(active), n_res=n_res, n_off=n_off, phase1_bytes=phase1, expert_weight_bytes=w_expert_all,
+                layer_bytes=layer, flops=flops, phase1_flops=4 * H * F * n_res + cfg.shared * 4 * H * cfg.shared_ffn * T)
+
+
+def cpu_baseline(layer, seconds: float):
+    """The CPU oracle (as it stands) on the same layer: whole batches until `seconds` have passed."""
+    import oracle
+    reps = 0
+    t0 = time.perf_counter()
+    while True:
+        oracle.layer_forward_synthetic(layer, offloaded=False)
+        reps += 1
+        el = time.perf_counter() - t0
+        if el >= seconds:
+            break
+    toks = reps * layer.cfg.tokens
+    return {"value": toks / el, "unit": "tokens/s", "cores": oracle.threads(), "kind": "oracle",
+            "sample": f"{reps} full batch(es) of {layer.cfg.tokens} tokens of the same layer (resident experts + "
+                      f"router + repack, fp64 C with OpenMP), {el:.1f} s"}
+
+
+def main() -> int:
+    ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=200)
+    ap.add_argument("--warmup", type=int, default=20)
+    ap.add_argument("--workload", default="c2_mixtral_decode")
+    ap.add_argument("--seed", type=int, default=0)
+    ap.add_argument("--copies", type=int, default=4, help="rotated expert-weight copies")
+    ap.add_argument("--cpu-seconds", type=float, default=10.0)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--calib-copy-mib", type=int, default=0,
+                    help="run one plain device copy of this many MiB first (counter calibration)")
+    args = ap.parse_args()
+
+    world = int(os.environ.get("WORLD_SIZE", "1"))
+    if args.gpus != 1 or world != 1:
+        print(json.dumps({"error": "this build measures one GPU only: the MoE-layer hot path runs on one "
+                                   "MI355X; multi-GPU sharding is a design note, not built"}), flush=True)
+        return 2
+
+    import numpy as np
+    import torch
+
+    import paper_2608_21614_amd as moe
+    from paper_2608_21614_amd.device import DeviceLayer, to_host
+    from workloads import CONFIGS, SyntheticLayer
+
+    cfg = CONFIGS[args.workload]
+    torch.cuda.set_device(0)
+    log(f"[bench] generating {args.workload} seed {args.seed}")
+    layer = SyntheticLayer(cfg, args.seed)
+    dev = DeviceLayer(layer)
+    copies = [(dev.w13, dev.w2)] + [(dev.w13.clone(), dev.w2.clone()) for _ in range(args.copies - 1)]
+    o = dev.alloc_outputs()
+    hip = moe.hip_runtime()
+    hip.hipEventCreateWithFlags.argtypes = [ctypes.POINTER(ctypes.c_void_p), ctypes.c_uint]
+    hip.hipEventElapsedTime.argtypes = [ctypes.POINTER(ctypes.c_float), ctypes.c_void_p, ctypes.c_void_p]
+    hip.hipEventSynchronize.argtypes = [ctypes.c_void_p]
+
+    def new_event():
+        ev = ctypes.c_void_p()
+        assert hip.hipEventCreateWithFlags(ctypes.byref(ev), 0) == 0
+        return ev
+
+    nE = moe.MOE_STAGE_EVENTS
+    ev = [(ctypes.c_void_p * nE)(*[new_event().value for _ in range(nE)]) for _ in range(args.steps)]
+
+    def make_args(i, events=None):
+        w13, w2 = copies[i % len(copies)]
+        dev.w13, dev.w2 = w13, w2
+        a = dev.args(o)
+        if events is not None:
+            a.stage_events = ctypes.cast(events, ctypes.POINTER(ctypes.c_void_p))
+        return a
+
+    plain = [make_args(i) for i in range(len(copies))]
+    timed = [make_args(i, ev[i]) for i in range(args.steps)]
+    stream = torch.cuda.current_stream()
+
+    if args.calib_copy_mib:
+        n = args.calib_copy_mib * (1 << 20) // 4
+        src = torch.ones(n, dtype=torch.float32, device="cuda")
+        dst = torch.empty_like(src)
+        torch.cuda.synchronize()
+        dst.copy_(src)
+        torch.cuda.synchronize()
+        log(f"[bench] calibration copy of {args.calib_copy_mib} MiB done")
+        del src, dst
+
+    for i in range(args.warmup):
+        moe.moe_layer_forward(plain[i % len(plain)], dev.ws, stream)
+    torch.cuda.synchronize()
+    log(f"[bench] warmup {args.warmup} done; timing {args.steps} steps")
+    t0 = time.perf_counter()
+    for i in range(args.steps):
+        moe.moe_layer_forward(timed[i], dev.ws, stream)
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+
+    stage_ms = np.zeros((args.steps, nE - 1))
+    f = ctypes.c_float()
+    for i in range(args.steps):
+        for j in range(nE - 1):
+            assert hip.hipEventElapsedTime(ctypes.byref(f), ev[i][j], ev[i][j + 1]) == 0
+            stage_ms[i, j] = f.value
+    assert hip.hipEventElapsedTime(ctypes.byref(f), ev[0][0], ev[-1][nE - 1]) == 0
+    event_span_ms = f.value
+    stage_us = {n: float(stage_ms[:, j].mean() * 1e3) for j, n in enumerate(STAGES)}
+
+    counts = to_host(o["counts"])
+    resident = (layer.expert_slot >= 0) & (layer.expert_slot < dev.slots)
+    alg = algorithmic_bytes(cfg, counts, resident)
+    ms_per_step = wall * 1e3 / args.steps
+    tokens_per_s = cfg.tokens / (ms_per_step * 1e-3)
+    p1_s = stage_us[DOMINANT] * 1e-6
+    achieved = alg["phase1_bytes"] / p1_s / 1e9
+    traffic = read_traffic(args.workload)
+    result = {
+        "metric": METRIC,
+        "value": tokens_per_s,
+        "unit": "tokens/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": ms_per_step,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16" if cfg.dtype == "bf16" else "f32",
+        "data": "synthetic (seeded: x ~ N(0,1), weights ~ N(0,0.02^2), bf16)",
+        "config": {"workload": args.workload, "description": cfg.description, "tokens": cfg.tokens,
+                   "hidden": cfg.hidden, "experts": cfg.experts, "ffn": cfg.ffn, "top_k": cfg.top_k,
+                   "shared": cfg.shared, "shared_ffn": cfg.shared_ffn, "resident_slots": dev.slots,
+                   "active_resident_experts": alg["active"], "resident_pairs": alg["n_res"],
+                   "offloaded_pairs": alg["n_off"], "seed": args.seed, "weight_copies": len(copies),
+                   "parallelism": "1 GPU"},
+        "hbm_gbps_expert_weights": alg["expert_weight_bytes"] / (ms_per_step * 1e-3) / 1e9,
+        "hbm_gbps_layer_algorithmic": alg["layer_bytes"] / (ms_per_step * 1e-3) / 1e9,
+        "stages_us": stage_us,
+        "event_span_ms_per_step": event_span_ms / args.steps,
+        "roofline": {
+            "kernel": "k_ffn_stream (phase 1: gate/up projections + SwiGLU)",
+            "bound": "hbm",
+            "achieved": achieved,
+            "peak": HBM_PEAK_GBPS,
+            "unit": "GB/s",
+            "frac": achieved / HBM_PEAK_GBPS,
+            "traffic": traffic,
+            "algorithmic_bytes_per_launch": alg["phase1_bytes"],
+            "mean_launch_us": stage_us[DOMINANT],
+        },
+    }
+    if not args.no_cpu_baseline:
+        log("[bench] timing the CPU oracle")
+        result["cpu_baseline"] = cpu_baseline(layer, args.cpu_seconds)
+    print(json.dumps(result), flush=True)
+    return 0
+
+
+if __name__ == "__main__":
+    sys.exit(main())

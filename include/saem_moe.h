@@ -27,15 +27,21 @@
  *     HIP; launch failures return MOE_ERR_HIP.
  *   - Calls on distinct streams with distinct workspaces may run concurrently.
  *   - Every tensor pointer must be 16-byte aligned (MOE_ERR_INVALID_ARG otherwise).
- *   - Layouts are row-major and K-contiguous:
- *       x          [T, H]        activations (dims.dtype)
- *       w_router   [E, H]        row e scores expert e (dims.dtype)
+ *   - Layouts:
+ *       x          [T, H]        activations (dims.dtype), row-major
+ *       w_router   [E, H]        row e scores expert e (dims.dtype), row-major
  *       bias       [E]           fp32 router bias, or NULL
- *       w13        [slots, 2F, H] per slot: rows 0..F-1 are the gate projection W1
- *                                (row f = output feature f), rows F..2F-1 the up
- *                                projection W3
- *       w2         [slots, H, F] per slot: row h = output feature h of W2
- *       ws13, ws2  [S, 2Fs, H], [S, H, Fs] shared experts, same layout
+ *       w13        [slots, 2F, H] per slot, in the TILE LAYOUT (moe_pack_weights):
+ *                                logical rows 0..F-1 are the gate projection W1
+ *                                (row f = output feature f), rows F..2F-1 the
+ *                                up projection W3, K = H
+ *       w2         [slots, H, F] per slot, tile layout: row h = output feature h
+ *                                of W2, K = F
+ *       ws13, ws2  [S, 2Fs, H], [S, H, Fs] shared experts, same tile layout
+ *     Tile layout of a logical [R, K] matrix: blocks of 16 rows x 32 columns;
+ *     block (rt, s) starts at element (rt * K/32 + s) * 512 and its element
+ *     8*l + i holds W[16*rt + l%16][32*s + 8*(l/16) + i].  Same size as the
+ *     row-major matrix.
  *   - Residency map: expert_slot[E] (int32, device).  Expert e is resident iff
  *     0 <= expert_slot[e] < dims.slots, and then its weights are
  *     w13[expert_slot[e]] and w2[expert_slot[e]]; any other value (e.g. -1)
@@ -193,7 +199,15 @@ typedef struct moe_layer_args {
     int32_t* n_res;              /* [1] */
     void* off_rows;              /* [T*k, H] dims.dtype, packed offloaded rows */
     float* off_w;                /* [T*k] */
+    /* optional stage timing: NULL, or MOE_STAGE_EVENTS hipEvent_t handles the
+     * caller created (timing enabled); the call records them on `stream`:
+     * [0] before routing, [1] after routing, [2] after repacking, [3] after the
+     * offloaded-row pack, [4] after FFN phase 1 (gate/up + SwiGLU), [5] after
+     * FFN phase 2 (down projection), [6] after the combine. */
+    void* const* stage_events;
 } moe_layer_args;
+
+#define MOE_STAGE_EVENTS 7
 
 /*
  * Fused forward of one MoE layer: route -> repack (+ offloaded pack) ->
@@ -203,6 +217,17 @@ typedef struct moe_layer_args {
  * merges with moe_combine(..., y_off, ...).  Needs moe_workspace_bytes(&dims).
  */
 moe_status moe_layer_forward(const moe_layer_args* args, void* ws, size_t ws_bytes, void* stream);
+
+/*
+ * Converts one row-major [rows, cols] expert matrix (cols contiguous) into the
+ * tile layout the FFN reads (see Layouts above).  Run once per expert when its
+ * weights are placed in a slot (fixed per-layer expert slots, Section IV-C.1);
+ * e.g. w13[slot] from the [2F, H] matrix whose row f is W1[:, f] and row F+f is
+ * W3[:, f], and w2[slot] from the [H, F] matrix whose row h is W2[:, h].
+ *   src, dst: device, distinct, rows * cols elements of `dtype` each.
+ *   rows % 16 == 0 and cols % 32 == 0, else MOE_ERR_UNSUPPORTED.
+ */
+moe_status moe_pack_weights(const void* src, void* dst, int64_t rows, int64_t cols, int32_t dtype, void* stream);
 
 /*
  * Stage-aware residency support (Section IV-B.2, Section IV-C.2).

@@ -66,8 +66,15 @@ def _load():
         lib.oracle_repack.restype = ctypes.c_int
         lib.oracle_expert_ffn.argtypes = [i64, i64, i64, ctypes.c_int, vp, ip, vp, vp, dp]
         lib.oracle_expert_ffn.restype = None
+        lib.oracle_threads.argtypes = []
+        lib.oracle_threads.restype = ctypes.c_int
         _lib = lib
     return _lib
+
+
+def threads() -> int:
+    """OpenMP threads the oracle's loops run on."""
+    return int(_load().oracle_threads())
 
 
 def _ptr(a: Optional[np.ndarray]):

@@ -28,6 +28,7 @@
  * plain sequential sum, so results do not depend on the thread count.
  */
 #include <math.h>
+#include <omp.h>
 #include <stdint.h>
 #include <stdlib.h>
 #include <string.h>
@@ -47,6 +48,9 @@ static double elem(const void* p, int64_t i, int dtype) {
 }
 
 int oracle_version(void) { return 1; }
+
+/* Threads the OpenMP loops below use. */
+int oracle_threads(void) { return omp_get_max_threads(); }
 
 /*
  * Router scores (Section II-A): score[t][e] = sum_h x[t][h] * w_router[e][h] + bias[e].

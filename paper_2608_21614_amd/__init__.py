@@ -20,11 +20,12 @@ LIB_PATH = os.path.join(HERE, "libsaem_moe.so")
 MOE_OK, MOE_ERR_INVALID_ARG, MOE_ERR_UNSUPPORTED, MOE_ERR_WORKSPACE, MOE_ERR_HIP = range(5)
 MOE_F32, MOE_BF16 = 0, 1
 MOE_LOGITS_IN = 1
+MOE_STAGE_EVENTS = 7
 
 EXPORTED = [
     "moe_abi_version", "moe_status_str", "moe_check_dims", "moe_workspace_bytes", "moe_route_topk",
     "moe_repack", "moe_grouped_ffn", "moe_combine", "moe_layer_forward", "moe_stage_accumulate",
-    "moe_stage_plan",
+    "moe_stage_plan", "moe_pack_weights",
 ]
 
 
@@ -50,14 +51,39 @@ class moe_layer_args(ctypes.Structure):
         ("ws13", _vp), ("ws2", _vp), ("out", _vp),
         ("logits", _vp), ("topk_idx", _vp), ("topk_w", _vp), ("counts", _vp), ("seg_start", _vp),
         ("perm", _vp), ("inv_perm", _vp), ("n_res", _vp), ("off_rows", _vp), ("off_w", _vp),
+        ("stage_events", ctypes.POINTER(ctypes.c_void_p)),
     ]
+
+
+def _mapped_hip_runtimes() -> set:
+    """Paths of every libamdhip64 mapped into this process."""
+    paths = set()
+    with open("/proc/self/maps") as f:
+        for line in f:
+            parts = line.split()
+            if len(parts) >= 6 and "libamdhip64" in parts[-1]:
+                paths.add(os.path.realpath(parts[-1]))
+    return paths
+
+
+def hip_runtime() -> ctypes.CDLL:
+    """The HIP runtime this process uses (the one torch loaded)."""
+    paths = _mapped_hip_runtimes()
+    if len(paths) != 1:
+        raise RuntimeError(f"expected exactly one HIP runtime in the process, found {sorted(paths)}")
+    return ctypes.CDLL(paths.pop())
 
 
 def _load() -> ctypes.CDLL:
     if not os.path.exists(LIB_PATH):
         raise ImportError(f"{LIB_PATH} is not built; run `python paper_2608_21614_amd/build.py` "
                           "(hipcc, gfx950) before using the HIP path")
+    # torch ships its own libamdhip64 (same soname); loading torch first makes the
+    # library bind to that copy, so both share one runtime, one set of streams.
+    import torch  # noqa: F401
     lib = ctypes.CDLL(LIB_PATH)
+    if len(_mapped_hip_runtimes()) != 1:
+        raise ImportError(f"two HIP runtimes in one process: {sorted(_mapped_hip_runtimes())}")
     D = ctypes.POINTER(moe_dims)
     i32, u32, sz = ctypes.c_int32, ctypes.c_uint32, ctypes.c_size_t
     sig = {
@@ -72,6 +98,7 @@ def _load() -> ctypes.CDLL:
         "moe_layer_forward": ([ctypes.POINTER(moe_layer_args), _vp, sz, _vp], ctypes.c_int),
         "moe_stage_accumulate": ([i32, _vp, _vp, _vp], ctypes.c_int),
         "moe_stage_plan": ([i32, i32, _vp, _vp, _vp], ctypes.c_int),
+        "moe_pack_weights": ([_vp, _vp, ctypes.c_int64, ctypes.c_int64, i32, _vp], ctypes.c_int),
     }
     for name, (args, res) in sig.items():
         fn = getattr(lib, name)
@@ -150,17 +177,31 @@ def moe_combine(dims, topk_idx, topk_w, inv_perm, expert_slot, y, y_off, n_res, 
 
 def layer_args(dims, x, w_router, bias, expert_slot, w13, w2, ws13, ws2, out, out_dtype: int, flags: int = 0,
                logits=None, topk_idx=None, topk_w=None, counts=None, seg_start=None, perm=None, inv_perm=None,
-               n_res=None, off_rows=None, off_w=None) -> moe_layer_args:
-    """Fills a moe_layer_args struct (kept alive by the caller while launches use it)."""
+               n_res=None, off_rows=None, off_w=None, stage_events=None) -> moe_layer_args:
+    """Fills a moe_layer_args struct (kept alive by the caller while launches use it).
+
+    stage_events: None, or a ctypes array of MOE_STAGE_EVENTS hipEvent_t handles.
+    """
     return moe_layer_args(
         ctypes.sizeof(moe_layer_args), dims, flags, out_dtype, _p(x), _p(w_router), _p(bias), _p(expert_slot),
         _p(w13), _p(w2), _p(ws13), _p(ws2), _p(out), _p(logits), _p(topk_idx), _p(topk_w), _p(counts),
-        _p(seg_start), _p(perm), _p(inv_perm), _p(n_res), _p(off_rows), _p(off_w))
+        _p(seg_start), _p(perm), _p(inv_perm), _p(n_res), _p(off_rows), _p(off_w),
+        ctypes.cast(stage_events, ctypes.POINTER(ctypes.c_void_p)) if stage_events is not None else None)
 
 
 def moe_layer_forward(args: moe_layer_args, ws, stream=None):
     _check(lib.moe_layer_forward(ctypes.byref(args), _p(ws), ws.numel() * ws.element_size(), _stream(stream)),
            "moe_layer_forward")
+
+
+def moe_pack_weights(src, dst, stream=None):
+    """Row-major [rows, cols] device matrix -> tile layout (same shape and dtype) in dst."""
+    import torch
+    if src.shape != dst.shape or src.dtype != dst.dtype or src.dim() < 2:
+        raise ValueError("moe_pack_weights: src and dst must have the same [.., rows, cols] shape and dtype")
+    dt = MOE_BF16 if src.dtype == torch.bfloat16 else MOE_F32
+    rows = src.numel() // src.shape[-1]
+    _check(lib.moe_pack_weights(_p(src), _p(dst), rows, src.shape[-1], dt, _stream(stream)), "moe_pack_weights")
 
 
 def moe_stage_accumulate(experts: int, counts, log, stream=None):

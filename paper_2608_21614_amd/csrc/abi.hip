@@ -231,10 +231,23 @@ moe_status moe_layer_forward(const moe_layer_args* a, void* ws, size_t ws_bytes,
     int32_t* inv = a->inv_perm ? a->inv_perm : at<int32_t>(ws, L.inv);
     int32_t* nres = a->n_res ? a->n_res : at<int32_t>(ws, L.nres);
 
-    hipError_t e = saem::launch_route_topk(s, a->x, a->w_router, lin ? nullptr : a->bias, logits, lin, idx, w, hs);
-    if (e == hipSuccess) e = saem::launch_repack(s, idx, a->expert_slot, counts, seg, perm, inv, nres, hs);
-    if (s.T == 0) return hip_status(e);
-    if (e == hipSuccess) e = saem::launch_offload_pack(s, a->x, w, perm, nres, a->off_rows, a->off_w, hs);
+    hipEvent_t ev[MOE_STAGE_EVENTS] = {};
+    if (a->stage_events)
+        for (int i = 0; i < MOE_STAGE_EVENTS; ++i) ev[i] = static_cast<hipEvent_t>(a->stage_events[i]);
+    auto mark = [&](hipError_t e, int i) {
+        if (e == hipSuccess && ev[i]) e = hipEventRecord(ev[i], hs);
+        return e;
+    };
+
+    hipError_t e = mark(hipSuccess, 0);
+    if (e == hipSuccess) e = mark(saem::launch_route_topk(s, a->x, a->w_router, lin ? nullptr : a->bias, logits, lin,
+                                                          idx, w, hs), 1);
+    if (e == hipSuccess) e = mark(saem::launch_repack(s, idx, a->expert_slot, counts, seg, perm, inv, nres, hs), 2);
+    if (s.T == 0) {
+        for (int i = 3; i < MOE_STAGE_EVENTS && e == hipSuccess; ++i) e = mark(hipSuccess, i);
+        return hip_status(e);
+    }
+    if (e == hipSuccess) e = mark(saem::launch_offload_pack(s, a->x, w, perm, nres, a->off_rows, a->off_w, hs), 3);
     saem::FfnArgs f;
     f.x = a->x; f.perm = perm; f.counts = counts; f.seg_start = seg; f.expert_slot = a->expert_slot;
     f.w13 = a->w13; f.w2 = a->w2; f.ws13 = a->ws13; f.ws2 = a->ws2;
@@ -243,11 +256,23 @@ moe_status moe_layer_forward(const moe_layer_args* a, void* ws, size_t ws_bytes,
     f.y = at<float>(ws, L.y);
     f.ks = L.ks;
     f.y_ks_stride = L.rows * (long long)s.H;
-    if (e == hipSuccess) e = saem::launch_grouped_ffn(s, f, hs);
+    if (e == hipSuccess) e = mark(saem::launch_grouped_ffn(s, f, hs, ev[4]), 5);
     if (e == hipSuccess)
-        e = saem::launch_combine(s, idx, w, inv, a->expert_slot, f.y, L.ks, f.y_ks_stride, nullptr, nullptr, a->out,
-                                 a->out_dtype == MOE_BF16, hs);
+        e = mark(saem::launch_combine(s, idx, w, inv, a->expert_slot, f.y, L.ks, f.y_ks_stride, nullptr, nullptr,
+                                      a->out, a->out_dtype == MOE_BF16, hs), 6);
     return hip_status(e);
+}
+
+moe_status moe_pack_weights(const void* src, void* dst, int64_t rows, int64_t cols, int32_t dtype, void* stream) {
+    if (dtype != MOE_F32 && dtype != MOE_BF16) return MOE_ERR_INVALID_ARG;
+    if (rows < 0 || cols < 0) return MOE_ERR_INVALID_ARG;
+    if (rows % 16 != 0 || cols % 32 != 0) return MOE_ERR_UNSUPPORTED;
+    const long long n = (long long)rows * cols;
+    if (!ok_arr(src, n) || !ok_arr(dst, n)) return MOE_ERR_INVALID_ARG;
+    const size_t bytes = (size_t)n * (dtype == MOE_BF16 ? 2 : 4);
+    const uintptr_t s0 = reinterpret_cast<uintptr_t>(src), d0 = reinterpret_cast<uintptr_t>(dst);
+    if (n > 0 && s0 < d0 + bytes && d0 < s0 + bytes) return MOE_ERR_INVALID_ARG;  // overlapping buffers
+    return hip_status(saem::launch_pack_weights(src, dst, rows, cols, dtype == MOE_BF16, static_cast<hipStream_t>(stream)));
 }
 
 moe_status moe_stage_accumulate(int32_t experts, const int32_t* counts, int64_t* log, void* stream) {

@@ -7,18 +7,26 @@
 //   phase 1: act[p, f] = silu(x[tok(p)] . W1[:,f]) * (x[tok(p)] . W3[:,f])
 //   phase 2: y[c][p, h] = sum over K chunk c of act[p, :] . W2[:,h]
 //
+// Expert weights are in the MFMA tile layout (pack.hip): a 16-row x 32-column
+// block is 1 KB of contiguous memory whose 64 16-byte pieces are the 64 lanes'
+// MFMA A operands.
+//
 // Three kernel families:
 //  * stream  (bf16, T <= 64, decode): the weights are streamed from HBM exactly
 //    once.  A workgroup owns 32 features (phase 1: 32 gate + 32 up weight
 //    rows) or 64 outputs (phase 2: 64 rows of W2) of one expert; the weights are
 //    the MFMA M side and the expert's tokens the N side, in tiles of 16.  Its
-//    four waves split K and their partial tiles are summed through LDS in wave
-//    order.  Phase 2 additionally splits K across workgroups into `ks` chunks
-//    whose partial sums the combine adds in fixed order.  SwiGLU is applied in
-//    the phase-1 epilogue, so gate and up projections are never stored.
+//    four waves split K interleaved -- wave w takes the 32-wide K steps w, w+4,
+//    w+8, ... -- so at any moment the workgroup reads 4 KB of contiguous memory
+//    per weight tile; each wave double-buffers its loads in registers (the next
+//    two K steps are in flight while the MFMAs of the current two run).  The
+//    waves' partial tiles are summed through LDS in wave order.  Phase 2 also
+//    splits K across workgroups into `ks` chunks whose partial sums the combine
+//    adds in fixed order.  SwiGLU is applied in the phase-1 epilogue, so the gate
+//    and up projections are never stored.
 //  * tiled   (bf16, T > 64, prefill): MFMA tiles of 64 weight rows x 64 tokens,
 //    K staged through LDS in double-buffered 64-wide slabs; the phase-1 tile
-//    interleaves 16 gate and 16 up rows per wave so SwiGLU runs in registers.
+//    holds 16 gate and 16 up rows per wave so SwiGLU runs in registers.
 //  * f32     (fp32 layers): plain fp32 FMA, one output per thread.
 // All of them read counts and offsets from device memory: the grid is sized for
 // the worst case on the host and surplus workgroups exit at once.
@@ -127,8 +135,8 @@ __device__ __forceinline__ int group_token(const Args& a, const Group& g, int n)
 
 template <int NT, bool kDown>
 __global__ void __launch_bounds__(256) k_ffn_stream(Args a) {
-    constexpr int MT = 4;                    // 16-row weight tiles per workgroup
-    constexpr int U = (NT <= 2) ? 4 : 2;     // K steps per load batch
+    constexpr int MT = 4;   // 16-row weight tiles per workgroup
+    constexpr int U = 2;    // K steps per load batch (two batches in flight)
     __shared__ int s_list[256];
     __shared__ int s_wsum[4];
     __shared__ f32x4 s_red[4][MT][NT][kWave];
@@ -154,34 +162,35 @@ __global__ void __launch_bounds__(256) k_ffn_stream(Args a) {
     const int wave = threadIdx.x >> 6, lane = lane_id();
     const int r = lane & 15, kq = (lane >> 4) * 8;
 
-    // weight rows of this workgroup and the K range of this wave
+    // weight tiles of this workgroup (16-row tiles in the tile layout) and the K chunk
     const uint16_t* wp[MT];
-    int row0, kc = 0, s0, s1;
+    int row0, kc = 0, c0, c1;
     if (!kDown) {
         const int f0 = sub * 32;
         row0 = f0;
+        const int nst = a.H / 32;
         const uint16_t* w = reinterpret_cast<const uint16_t*>(g.w13);
 #pragma unroll
         for (int m = 0; m < MT; ++m) {
-            const int feat = f0 + 16 * (m & 1) + r;
-            const int row = (m < 2) ? feat : g.Fg + feat;
-            wp[m] = w + (size_t)row * a.H + kq;
+            const int rt = (m < 2 ? 0 : g.Fg / 16) + f0 / 16 + (m & 1);  // gate tiles, then up tiles
+            wp[m] = w + (size_t)rt * nst * 512 + lane * 8;
         }
-        const int nsteps = a.H / 32;
-        s0 = wave * nsteps / 4;
-        s1 = (wave + 1) * nsteps / 4;
+        c0 = 0;
+        c1 = nst;
     } else {
         const int h0 = (sub / a.ks) * 64;
         kc = sub % a.ks;
         row0 = h0;
+        const int nst = g.Fg / 32;
         const uint16_t* w = reinterpret_cast<const uint16_t*>(g.w2);
 #pragma unroll
-        for (int m = 0; m < MT; ++m) wp[m] = w + (size_t)(h0 + 16 * m + r) * g.Fg + kq;
-        const int nsteps = g.Fg / 32;
-        const int c0 = kc * nsteps / a.ks, c1 = (kc + 1) * nsteps / a.ks;
-        s0 = c0 + wave * (c1 - c0) / 4;
-        s1 = c0 + (wave + 1) * (c1 - c0) / 4;
+        for (int m = 0; m < MT; ++m) wp[m] = w + (size_t)(h0 / 16 + m) * nst * 512 + lane * 8;
+        c0 = kc * nst / a.ks;
+        c1 = (kc + 1) * nst / a.ks;
     }
+    // this wave's K steps: c0 + wave + 4 i
+    const int n_my = (c1 - c0 > wave) ? (c1 - c0 - wave + 3) / 4 : 0;
+    const int sbase = c0 + wave;
 
     // token operand rows (N side)
     const int ntile = min(NT, (g.count + 15) / 16);
@@ -204,16 +213,18 @@ __global__ void __launch_bounds__(256) k_ffn_stream(Args a) {
 #pragma unroll
         for (int j = 0; j < NT; ++j) acc[m][j] = f32x4{0.f, 0.f, 0.f, 0.f};
 
-    int s = s0;
-    for (; s + U <= s1; s += U) {
-        bf16x8 A[U][MT], B[U][NT];
+    // batch b holds this wave's steps i = U*b .. U*b+U-1
+    auto load = [&](bf16x8 (&A)[U][MT], bf16x8 (&B)[U][NT], int b) {
 #pragma unroll
         for (int u = 0; u < U; ++u) {
+            const int s = sbase + 4 * (U * b + u);
 #pragma unroll
-            for (int m = 0; m < MT; ++m) A[u][m] = load_bf16x8_stream(wp[m] + (s + u) * 32);
+            for (int m = 0; m < MT; ++m) A[u][m] = load_bf16x8(wp[m] + (size_t)s * 512);
 #pragma unroll
-            for (int j = 0; j < NT; ++j) B[u][j] = (j < ntile && bp[j]) ? load_bf16x8(bp[j] + (s + u) * 32) : zero_bf16x8();
+            for (int j = 0; j < NT; ++j) B[u][j] = (j < ntile && bp[j]) ? load_bf16x8(bp[j] + s * 32) : zero_bf16x8();
         }
+    };
+    auto mma = [&](const bf16x8 (&A)[U][MT], const bf16x8 (&B)[U][NT]) {
 #pragma unroll
         for (int u = 0; u < U; ++u)
 #pragma unroll
@@ -221,11 +232,23 @@ __global__ void __launch_bounds__(256) k_ffn_stream(Args a) {
                 if (j < ntile)
 #pragma unroll
                     for (int m = 0; m < MT; ++m) acc[m][j] = mfma16x16x32(A[u][m], B[u][j], acc[m][j]);
+    };
+    const int nb = n_my / U;
+    {
+        bf16x8 A0[U][MT], B0[U][NT], A1[U][MT], B1[U][NT];
+        if (nb > 0) load(A0, B0, 0);
+        for (int b = 0; b < nb; b += 2) {
+            if (b + 1 < nb) load(A1, B1, b + 1);
+            mma(A0, B0);
+            if (b + 2 < nb) load(A0, B0, b + 2);
+            if (b + 1 < nb) mma(A1, B1);
+        }
     }
-    for (; s < s1; ++s) {
+    for (int i = nb * U; i < n_my; ++i) {
+        const int s = sbase + 4 * i;
         bf16x8 A[MT], B[NT];
 #pragma unroll
-        for (int m = 0; m < MT; ++m) A[m] = load_bf16x8_stream(wp[m] + s * 32);
+        for (int m = 0; m < MT; ++m) A[m] = load_bf16x8(wp[m] + (size_t)s * 512);
 #pragma unroll
         for (int j = 0; j < NT; ++j) B[j] = (j < ntile && bp[j]) ? load_bf16x8(bp[j] + s * 32) : zero_bf16x8();
 #pragma unroll
@@ -283,7 +306,6 @@ __global__ void __launch_bounds__(256) k_ffn_stream(Args a) {
 // tiled kernel (prefill)
 // ---------------------------------------------------------------------------
 
-constexpr int kTm = 64;      // weight rows per tile
 constexpr int kTn = 64;      // tokens per tile
 constexpr int kTk = 64;      // K slab
 constexpr int kPitch = kTk + 8;  // LDS row pitch (bf16 elements)
@@ -330,7 +352,7 @@ __global__ void __launch_bounds__(256) k_ffn_tiled(Args a, int max_rtiles, int n
     __shared__ int s_list[256];
     __shared__ int s_wsum[4];
     __shared__ int s_tpre[260];
-    __shared__ __attribute__((aligned(16))) uint16_t sW[2][kTm][kPitch];
+    __shared__ __attribute__((aligned(16))) uint16_t sW[2][8][512];
     __shared__ __attribute__((aligned(16))) uint16_t sX[2][kTn][kPitch];
 
     const int nact = list_active(a, s_list, s_wsum);
@@ -366,27 +388,35 @@ __global__ void __launch_bounds__(256) k_ffn_tiled(Args a, int max_rtiles, int n
     const int tid = threadIdx.x, wave = tid >> 6, lane = lane_id();
     const int K = kDown ? g.Fg : a.H;
     const uint16_t* wbase = reinterpret_cast<const uint16_t*>(kDown ? g.w2 : g.w13);
-    const int ldw = kDown ? g.Fg : a.H;
     const int wrow0 = wn * (kDown ? 64 : 32);  // first output feature (phase 1) or output row (phase 2)
 
-    // global -> LDS copy assignment: 512 chunks of 16 B per tile, 2 per thread
+    // global -> LDS copy assignment, 2 chunks of 16 B per thread per tile:
+    // W: 8 blocks of 1 KB (4 row tiles x 2 K steps of the 64-wide slab), copied as is;
+    // X: 64 token rows x 64 columns.
+    const int nst = K / 32;
+    int rt_of[4];
+    if (!kDown) {
+        const int t0 = wrow0 / 16;  // wrow0 = first feature of the tile
+        rt_of[0] = t0;
+        rt_of[1] = t0 + 1;
+        rt_of[2] = g.Fg / 16 + t0;
+        rt_of[3] = g.Fg / 16 + t0 + 1;
+    } else {
+#pragma unroll
+        for (int i = 0; i < 4; ++i) rt_of[i] = wrow0 / 16 + i;
+    }
     const uint16_t* gW[2];
     const uint16_t* gX[2];
-    int cr[2], cc[2];
+    int wb[2], wl[2], cr[2], cc[2];
 #pragma unroll
     for (int i = 0; i < 2; ++i) {
         const int c = tid + 256 * i;
+        wb[i] = c >> 6;
+        wl[i] = c & 63;
+        const int rtl = wb[i] >> 1, ks = wb[i] & 1;
+        gW[i] = wbase + ((size_t)rt_of[rtl] * nst + ks) * 512 + wl[i] * 8;
         cr[i] = c >> 3;
         cc[i] = (c & 7) * 8;
-        int row;
-        if (!kDown) {
-            const int half = cr[i] >> 5, sub = cr[i] & 31;
-            const int feat = wrow0 + 16 * half + (sub & 15);
-            row = (sub < 16) ? feat : g.Fg + feat;
-        } else {
-            row = wrow0 + cr[i];
-        }
-        gW[i] = wbase + (size_t)row * ldw + cc[i];
         const int n = n0 + cr[i];
         gX[i] = nullptr;
         if (!kDown) {
@@ -410,14 +440,14 @@ __global__ void __launch_bounds__(256) k_ffn_tiled(Args a, int max_rtiles, int n
     auto gload = [&](int kt) {
 #pragma unroll
         for (int i = 0; i < 2; ++i) {
-            rw[i] = *reinterpret_cast<const u32x4*>(gW[i] + kt * kTk);
+            rw[i] = *reinterpret_cast<const u32x4*>(gW[i] + (size_t)kt * 2 * 512);
             rx[i] = gX[i] ? *reinterpret_cast<const u32x4*>(gX[i] + kt * kTk) : u32x4{0u, 0u, 0u, 0u};
         }
     };
     auto lstore = [&](int buf) {
 #pragma unroll
         for (int i = 0; i < 2; ++i) {
-            *reinterpret_cast<u32x4*>(&sW[buf][cr[i]][cc[i]]) = rw[i];
+            *reinterpret_cast<u32x4*>(&sW[buf][wb[i]][wl[i] * 8]) = rw[i];
             *reinterpret_cast<u32x4*>(&sX[buf][cr[i]][cc[i]]) = rx[i];
         }
     };
@@ -432,8 +462,11 @@ __global__ void __launch_bounds__(256) k_ffn_tiled(Args a, int max_rtiles, int n
         for (int ks = 0; ks < kTk / 32; ++ks) {
             bf16x8 A[2], B[2];
 #pragma unroll
-            for (int m = 0; m < 2; ++m)
-                A[m] = __builtin_bit_cast(bf16x8, *reinterpret_cast<const u32x4*>(&sW[buf][32 * wr + 16 * m + r][ks * 32 + kq]));
+            for (int m = 0; m < 2; ++m) {
+                // phase 1: gate tile wr and up tile wr (same features); phase 2: tiles 2wr, 2wr+1
+                const int rtl = kDown ? 2 * wr + m : (m == 0 ? wr : 2 + wr);
+                A[m] = __builtin_bit_cast(bf16x8, *reinterpret_cast<const u32x4*>(&sW[buf][rtl * 2 + ks][lane * 8]));
+            }
 #pragma unroll
             for (int j = 0; j < 2; ++j)
                 B[j] = __builtin_bit_cast(bf16x8, *reinterpret_cast<const u32x4*>(&sX[buf][32 * wc + 16 * j + r][ks * 32 + kq]));
@@ -472,6 +505,11 @@ __global__ void __launch_bounds__(256) k_ffn_tiled(Args a, int max_rtiles, int n
 // fp32 kernels
 // ---------------------------------------------------------------------------
 
+// Element (row, k) of a [R, K] matrix stored in the tile layout.
+__device__ __forceinline__ size_t tile_off(int row, int k, int K) {
+    return ((size_t)(row >> 4) * (K >> 5) + (k >> 5)) * 512 + ((k & 31) >> 3) * 128 + (row & 15) * 8 + (k & 7);
+}
+
 __device__ bool resolve_group_f32(const Args& a, int gidx, int* s_list, int* s_wsum, Group* g) {
     const int nact = list_active(a, s_list, s_wsum);
     if (gidx < a.max_routed) {
@@ -493,8 +531,7 @@ __global__ void __launch_bounds__(256) k_ffn1_f32(Args a) {
     const int f = blockIdx.y * 64 + (threadIdx.x & 63);
     if (f >= g.Fg) return;
     const float* x = static_cast<const float*>(a.x);
-    const float* wg = reinterpret_cast<const float*>(g.w13) + (size_t)f * a.H;
-    const float* wu = reinterpret_cast<const float*>(g.w13) + (size_t)(g.Fg + f) * a.H;
+    const float* w13 = reinterpret_cast<const float*>(g.w13);
     float* act = static_cast<float*>(a.act);
     for (int n = threadIdx.x >> 6; n < g.count; n += 4) {
         const int t = group_token(a, g, n);
@@ -502,8 +539,8 @@ __global__ void __launch_bounds__(256) k_ffn1_f32(Args a) {
         const float* xr = x + (size_t)t * a.H;
         float gs = 0.f, us = 0.f;
         for (int h = 0; h < a.H; ++h) {
-            gs = fmaf(xr[h], wg[h], gs);
-            us = fmaf(xr[h], wu[h], us);
+            gs = fmaf(xr[h], w13[tile_off(f, h, a.H)], gs);
+            us = fmaf(xr[h], w13[tile_off(g.Fg + f, h, a.H)], us);
         }
         act[(size_t)(g.rowbase + n) * a.Fa + f] = silu(gs) * us;
     }
@@ -516,12 +553,12 @@ __global__ void __launch_bounds__(256) k_ffn2_f32(Args a) {
     if (!resolve_group_f32(a, blockIdx.x, s_list, s_wsum, &g)) return;
     const int h = blockIdx.y * 64 + (threadIdx.x & 63);
     if (h >= a.H) return;
-    const float* w = reinterpret_cast<const float*>(g.w2) + (size_t)h * g.Fg;
+    const float* w2 = reinterpret_cast<const float*>(g.w2);
     const float* act = static_cast<const float*>(a.act);
     for (int n = threadIdx.x >> 6; n < g.count; n += 4) {
         const float* ar = act + (size_t)(g.rowbase + n) * a.Fa;
         float s = 0.f;
-        for (int f = 0; f < g.Fg; ++f) s = fmaf(ar[f], w[f], s);
+        for (int f = 0; f < g.Fg; ++f) s = fmaf(ar[f], w2[tile_off(h, f, g.Fg)], s);
         a.y[(size_t)(g.rowbase + n) * a.H + h] = s;
     }
 }
@@ -573,8 +610,13 @@ int ffn_down_splits(const Shape& s) {
     return ks;
 }
 
-hipError_t launch_grouped_ffn(const Shape& s, const FfnArgs& fa, hipStream_t st) {
+hipError_t launch_grouped_ffn(const Shape& s, const FfnArgs& fa, hipStream_t st, hipEvent_t between) {
     if (s.T == 0) return hipSuccess;
+    auto mark = [&]() -> hipError_t {
+        hipError_t e = hipGetLastError();
+        if (e == hipSuccess && between) e = hipEventRecord(between, st);
+        return e;
+    };
     Args a;
     a.T = s.T; a.H = s.H; a.E = s.E; a.F = s.F; a.k = s.k; a.S = s.S; a.Fs = s.Fs; a.slots = s.slots;
     a.x = fa.x; a.perm = fa.perm; a.counts = fa.counts; a.seg_start = fa.seg_start; a.expert_slot = fa.expert_slot;
@@ -587,6 +629,7 @@ hipError_t launch_grouped_ffn(const Shape& s, const FfnArgs& fa, hipStream_t st)
         if (groups == 0) return hipSuccess;
         const int fmax = s.S > 0 && s.Fs > s.F ? s.Fs : s.F;
         hipLaunchKernelGGL(k_ffn1_f32, dim3(groups, fmax / 64), dim3(256), 0, st, a);
+        if (hipError_t e = mark(); e != hipSuccess) return e;
         hipLaunchKernelGGL(k_ffn2_f32, dim3(groups, s.H / 64), dim3(256), 0, st, a);
         return hipGetLastError();
     }
@@ -604,6 +647,7 @@ hipError_t launch_grouped_ffn(const Shape& s, const FfnArgs& fa, hipStream_t st)
                 default: hipLaunchKernelGGL((k_ffn_stream<4, false>), dim3(grid), dim3(256), 0, st, a); break;
             }
         }
+        if (hipError_t e = mark(); e != hipSuccess) return e;
         // phase 2: 64 output rows x one K chunk per workgroup
         a.ipg_r = (s.H / 64) * a.ks;
         a.ipg_s = (s.H / 64) * a.ks;
@@ -628,6 +672,7 @@ hipError_t launch_grouped_ffn(const Shape& s, const FfnArgs& fa, hipStream_t st)
         const long long grid = (long long)max_rtiles * ntn_r + (long long)s.S * tps * ntn_s;
         if (grid > 0) hipLaunchKernelGGL((k_ffn_tiled<false>), dim3((unsigned)grid), dim3(256), 0, st, a, max_rtiles, ntn_r, ntn_s > 0 ? ntn_s : 1);
     }
+    if (hipError_t e = mark(); e != hipSuccess) return e;
     {
         const int ntn = s.H / 64;
         const long long grid = (long long)max_rtiles * ntn + (long long)s.S * tps * ntn;

@@ -45,7 +45,8 @@ struct FfnArgs {
 
 // Number of K chunks the down projection is split into (1 = direct sums).
 int ffn_down_splits(const Shape& s);
-hipError_t launch_grouped_ffn(const Shape& s, const FfnArgs& a, hipStream_t st);
+// Launches phase 1 then phase 2; records `between` (if not null) after phase 1.
+hipError_t launch_grouped_ffn(const Shape& s, const FfnArgs& a, hipStream_t st, hipEvent_t between = nullptr);
 
 // y_out[p] = sum_c y[c][p] for the resident packed rows and the shared rows.
 hipError_t launch_reduce_splits(const Shape& s, const int32_t* counts, const int32_t* expert_slot, const float* y,
@@ -55,6 +56,9 @@ hipError_t launch_reduce_splits(const Shape& s, const int32_t* counts, const int
 hipError_t launch_combine(const Shape& s, const int32_t* topk_idx, const float* topk_w, const int32_t* inv_perm,
                           const int32_t* expert_slot, const float* y, int ks, long long y_ks_stride,
                           const float* y_off, const int32_t* n_res, void* out, bool out_bf16, hipStream_t st);
+
+// Row-major [rows, K] -> tile layout.
+hipError_t launch_pack_weights(const void* src, void* dst, long long rows, long long K, bool bf16, hipStream_t st);
 
 hipError_t launch_stage_accumulate(int E, const int32_t* counts, int64_t* log, hipStream_t st);
 

@@ -1,9 +1,9 @@
 """Device-side buffers of one synthetic MoE layer and a fused-forward runner.
 
 Plumbing only: uploads the seeded host tensors of a ``workloads.SyntheticLayer``
-to HBM as torch tensors (slot-major expert weights), allocates the outputs and
-the workspace once, and calls ``moe_layer_forward``.  No arithmetic of the layer
-happens here.
+to HBM as torch tensors, packs each resident expert's weights into its slot in
+the tile layout (``moe_pack_weights``), allocates the outputs and the workspace
+once, and calls ``moe_layer_forward``.  No arithmetic of the layer happens here.
 """
 from __future__ import annotations
 
@@ -12,7 +12,8 @@ from typing import Dict, Optional
 import numpy as np
 import torch
 
-from . import (MOE_BF16, MOE_F32, MOE_LOGITS_IN, layer_args, make_dims, moe_layer_forward, moe_workspace_bytes)
+from . import (MOE_BF16, MOE_F32, MOE_LOGITS_IN, layer_args, make_dims, moe_layer_forward, moe_pack_weights,
+               moe_workspace_bytes)
 
 
 def to_device(a: np.ndarray, device="cuda") -> torch.Tensor:
@@ -51,15 +52,15 @@ class DeviceLayer:
         self.w13 = torch.empty((max(self.slots, 1), 2 * F, H), dtype=self.tdtype, device=device)
         self.w2 = torch.empty((max(self.slots, 1), H, F), dtype=self.tdtype, device=device)
         for s, e in enumerate(se):
-            self.w13[s].copy_(to_device(layer.w13(int(e)), device))
-            self.w2[s].copy_(to_device(layer.w2(int(e)), device))
+            moe_pack_weights(to_device(layer.w13(int(e)), device), self.w13[s])
+            moe_pack_weights(to_device(layer.w2(int(e)), device), self.w2[s])
         if c.shared > 0:
             Fs = c.shared_ffn
             self.ws13 = torch.empty((c.shared, 2 * Fs, H), dtype=self.tdtype, device=device)
             self.ws2 = torch.empty((c.shared, H, Fs), dtype=self.tdtype, device=device)
             for s in range(c.shared):
-                self.ws13[s].copy_(to_device(layer.ws13(s), device))
-                self.ws2[s].copy_(to_device(layer.ws2(s), device))
+                moe_pack_weights(to_device(layer.ws13(s), device), self.ws13[s])
+                moe_pack_weights(to_device(layer.ws2(s), device), self.ws2[s])
         else:
             self.ws13 = self.ws2 = None
         self.dims = make_dims(c.tokens, c.hidden, c.experts, c.ffn, c.top_k, c.shared, c.shared_ffn if c.shared else 0,

@@ -129,6 +129,12 @@ def test_invalid_pointers_rejected_before_any_launch(pkg):
     # shared experts declared but no shared weights
     d2 = ctypes.byref(pkg.make_dims(**dict(GOOD, shared=1, shared_ffn=128)))
     assert lib.moe_grouped_ffn(d2, f, f, f, f, f, f, f, None, None, f, f, 1 << 40, None) == 1
+    # pack: shapes not multiples of (16, 32), overlapping buffers, bad dtype
+    assert lib.moe_pack_weights(f, _fake(0x90000000), 17, 32, 1, None) == 2
+    assert lib.moe_pack_weights(f, _fake(0x90000000), 16, 48, 1, None) == 2
+    assert lib.moe_pack_weights(f, _fake(0x10000 + 256), 16, 32, 1, None) == 1
+    assert lib.moe_pack_weights(f, _fake(0x90000000), 16, 32, 5, None) == 1
+    assert lib.moe_pack_weights(None, _fake(0x90000000), 16, 32, 1, None) == 1
     # stage accumulate
     assert lib.moe_stage_accumulate(0, f, f, None) == 1
     assert lib.moe_stage_accumulate(8, None, f, None) == 1

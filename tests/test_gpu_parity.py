@@ -47,6 +47,30 @@ def x_as_f32(layer):
 
 
 # ---------------------------------------------------------------------------
+# weight packing into the tile layout
+# ---------------------------------------------------------------------------
+
+@pytest.mark.parametrize("rows,cols,dtype", [(16, 32, "bf16"), (2816, 2048, "bf16"), (64, 1408, "bf16"),
+                                            (128, 256, "f32"), (48, 96, "f32")])
+def test_pack_weights_layout(moe, rows, cols, dtype):
+    """Packed element 8*l + i of block (rt, s) is W[16 rt + l%16][32 s + 8 (l/16) + i]; the inverse recovers W."""
+    say("pack", rows, cols, dtype)
+    rng = np.random.default_rng(rows + cols)
+    w = rng.integers(0, 1 << 16, size=(rows, cols), dtype=np.uint16) if dtype == "bf16" else \
+        rng.standard_normal((rows, cols)).astype(np.float32)
+    src = _dev(w)
+    dst = torch.empty_like(src)
+    moe.moe_pack_weights(src, dst)
+    torch.cuda.synchronize()
+    got = _host(dst).reshape(rows // 16, cols // 32, 4, 16, 8)
+    back = got.transpose(0, 3, 1, 2, 4).reshape(rows, cols)
+    np.testing.assert_array_equal(back, w)
+    # one explicit element
+    rt, s_, l, i = rows // 16 - 1, cols // 32 - 1, 37, 5
+    assert _host(dst).reshape(-1)[(rt * (cols // 32) + s_) * 512 + 8 * l + i] == w[16 * rt + l % 16, 32 * s_ + 8 * (l // 16) + i]
+
+
+# ---------------------------------------------------------------------------
 # routing on given scores: bit-exact selection
 # ---------------------------------------------------------------------------
 
