@@ -118,9 +118,11 @@ moe_status moe_workspace_bytes(const moe_dims* dims, size_t* bytes);
  *   topk_w  [T,k] fp32: softmax of the k selected scores (renormalised gate);
  *           a selected score equal to the top one contributes exactly 1, so a
  *           row of equal scores (also all -inf) gets 1/k.  NaN scores: undefined.
+ *   ws:     workspace of moe_workspace_bytes(dims) bytes (partial scores).
  */
 moe_status moe_route_topk(const moe_dims* dims, const void* x, const void* w_router, const float* bias,
-                          float* logits, uint32_t flags, int32_t* topk_idx, float* topk_w, void* stream);
+                          float* logits, uint32_t flags, int32_t* topk_idx, float* topk_w, void* ws, size_t ws_bytes,
+                          void* stream);
 
 /*
  * Expert-aligned token repacking with the residency split (Section IV-E.1,

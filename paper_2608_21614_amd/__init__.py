@@ -91,7 +91,7 @@ def _load() -> ctypes.CDLL:
         "moe_status_str": ([ctypes.c_int], ctypes.c_char_p),
         "moe_check_dims": ([D], ctypes.c_int),
         "moe_workspace_bytes": ([D, ctypes.POINTER(ctypes.c_size_t)], ctypes.c_int),
-        "moe_route_topk": ([D, _vp, _vp, _vp, _vp, u32, _vp, _vp, _vp], ctypes.c_int),
+        "moe_route_topk": ([D, _vp, _vp, _vp, _vp, u32, _vp, _vp, _vp, sz, _vp], ctypes.c_int),
         "moe_repack": ([D, _vp, _vp, _vp, _vp, _vp, _vp, _vp, _vp, _vp, _vp, _vp, _vp], ctypes.c_int),
         "moe_grouped_ffn": ([D, _vp, _vp, _vp, _vp, _vp, _vp, _vp, _vp, _vp, _vp, _vp, sz, _vp], ctypes.c_int),
         "moe_combine": ([D, _vp, _vp, _vp, _vp, _vp, _vp, _vp, _vp, i32, _vp], ctypes.c_int),
@@ -151,10 +151,10 @@ def moe_workspace_bytes(dims: moe_dims) -> int:
     return int(n.value)
 
 
-def moe_route_topk(dims, x, w_router, bias, logits, topk_idx, topk_w, logits_in: bool = False, stream=None):
+def moe_route_topk(dims, x, w_router, bias, logits, topk_idx, topk_w, ws, logits_in: bool = False, stream=None):
     _check(lib.moe_route_topk(ctypes.byref(dims), _p(x), _p(w_router), _p(bias), _p(logits),
-                              MOE_LOGITS_IN if logits_in else 0, _p(topk_idx), _p(topk_w), _stream(stream)),
-           "moe_route_topk")
+                              MOE_LOGITS_IN if logits_in else 0, _p(topk_idx), _p(topk_w), _p(ws),
+                              ws.numel() * ws.element_size(), _stream(stream)), "moe_route_topk")
 
 
 def moe_repack(dims, topk_idx, topk_w, expert_slot, x, counts, seg_start, perm, inv_perm, n_res,

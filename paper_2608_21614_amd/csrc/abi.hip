@@ -54,7 +54,7 @@ Shape shape_of(const moe_dims* d) {
 
 // Workspace layout (256-byte aligned regions).
 struct Layout {
-    size_t logits, idx, w, counts, seg, nres, perm, inv, act, y, total;
+    size_t logits, idx, w, counts, seg, nres, perm, inv, part, act, y, total;
     int ks, Fa;
     long long rows;
 };
@@ -81,6 +81,7 @@ Layout layout_of(const Shape& s) {
     L.nres = take(4);
     L.perm = take(T * k * 4);
     L.inv = take(T * k * 4);
+    L.part = take((size_t)saem::router_slices(s) * 64 * E * 4);
     L.act = take((size_t)L.rows * L.Fa * (s.bf16 ? 2 : 4));
     L.y = take((size_t)L.ks * L.rows * H * 4);
     L.total = off;
@@ -122,7 +123,8 @@ moe_status moe_workspace_bytes(const moe_dims* dims, size_t* bytes) {
 }
 
 moe_status moe_route_topk(const moe_dims* dims, const void* x, const void* w_router, const float* bias,
-                          float* logits, uint32_t flags, int32_t* topk_idx, float* topk_w, void* stream) {
+                          float* logits, uint32_t flags, int32_t* topk_idx, float* topk_w, void* ws, size_t ws_bytes,
+                          void* stream) {
     moe_status st = check_dims(dims);
     if (st != MOE_OK) return st;
     if (flags & ~MOE_LOGITS_IN) return MOE_ERR_INVALID_ARG;
@@ -131,8 +133,10 @@ moe_status moe_route_topk(const moe_dims* dims, const void* x, const void* w_rou
     if (!ok_arr(logits, T) || !ok_arr(topk_idx, T) || !ok_arr(topk_w, T)) return MOE_ERR_INVALID_ARG;
     if (!lin && (!ok_arr(x, T) || !ok_ptr(w_router) || !ok_opt(bias))) return MOE_ERR_INVALID_ARG;
     const Shape s = shape_of(dims);
+    const Layout L = layout_of(s);
+    if (!ws || ws_bytes < L.total || !aligned16(ws)) return MOE_ERR_WORKSPACE;
     return hip_status(saem::launch_route_topk(s, x, w_router, lin ? nullptr : bias, logits, lin, topk_idx, topk_w,
-                                              static_cast<hipStream_t>(stream)));
+                                              at<float>(ws, L.part), static_cast<hipStream_t>(stream)));
 }
 
 moe_status moe_repack(const moe_dims* dims, const int32_t* topk_idx, const float* topk_w,
@@ -240,15 +244,35 @@ moe_status moe_layer_forward(const moe_layer_args* a, void* ws, size_t ws_bytes,
     };
 
     hipError_t e = mark(hipSuccess, 0);
-    if (e == hipSuccess) e = mark(saem::launch_route_topk(s, a->x, a->w_router, lin ? nullptr : a->bias, logits, lin,
-                                                          idx, w, hs), 1);
-    if (e == hipSuccess) e = mark(saem::launch_repack(s, idx, a->expert_slot, counts, seg, perm, inv, nres, hs), 2);
+    if (saem::front_small_fits(s)) {
+        // one workgroup routes and repacks a decode batch; both stage events mark its end
+        if (e == hipSuccess)
+            e = mark(saem::launch_front_small(s, a->x, a->w_router, lin ? nullptr : a->bias, logits, lin, idx, w,
+                                              at<float>(ws, L.part), a->expert_slot, counts, seg, perm, inv, nres, hs),
+                     1);
+        if (e == hipSuccess) e = mark(hipSuccess, 2);
+    } else {
+        if (e == hipSuccess)
+            e = mark(saem::launch_route_topk(s, a->x, a->w_router, lin ? nullptr : a->bias, logits, lin, idx, w,
+                                             nullptr, hs),
+                     1);
+        if (e == hipSuccess) e = mark(saem::launch_repack(s, idx, a->expert_slot, counts, seg, perm, inv, nres, hs), 2);
+    }
     if (s.T == 0) {
         for (int i = 3; i < MOE_STAGE_EVENTS && e == hipSuccess; ++i) e = mark(hipSuccess, i);
         return hip_status(e);
     }
-    if (e == hipSuccess) e = mark(saem::launch_offload_pack(s, a->x, w, perm, nres, a->off_rows, a->off_w, hs), 3);
+    const bool fold_pack = saem::ffn_packs_offloaded(s);
+    if (e == hipSuccess)
+        e = mark(fold_pack ? hipSuccess
+                           : saem::launch_offload_pack(s, a->x, w, perm, nres, a->off_rows, a->off_w, hs), 3);
     saem::FfnArgs f;
+    if (fold_pack) {
+        f.topk_w = w;
+        f.n_res = nres;
+        f.off_rows = a->off_rows;
+        f.off_w = a->off_w;
+    }
     f.x = a->x; f.perm = perm; f.counts = counts; f.seg_start = seg; f.expert_slot = a->expert_slot;
     f.w13 = a->w13; f.w2 = a->w2; f.ws13 = a->ws13; f.ws2 = a->ws2;
     f.act = at<char>(ws, L.act);

@@ -1,0 +1,271 @@
+// block_ops.hpp -- workgroup-level building blocks of the routing front end:
+// router scores on MFMA, the wave-wide top-k gate, and the single-workgroup
+// counting sort that repacks the (token, expert) pairs.
+#pragma once
+
+#include <math.h>
+
+#include "common.hpp"
+
+namespace saem {
+
+constexpr int kFrontThreads = 1024;            // 16 waves
+constexpr int kFrontWaves = kFrontThreads / kWave;
+constexpr int kLgPitch = 257;                   // LDS row pitch of a score tile (E <= 256)
+constexpr int kScoreChunk = 64;                 // experts (4 MFMA row tiles) per reduction pass
+
+// Top-k of one token's scores held as v[i] = score of expert lane + 64 i (one wave).
+// Selection order: higher score first, equal scores -> lower expert id.  Writes
+// out_idx[0..k), out_w[0..k) (softmax over the selected scores) and, if given,
+// lds_idx[0..k).
+__device__ inline void topk_wave(const float (&v)[4], int E, int k, int32_t* out_idx, float* out_w, int32_t* lds_idx) {
+    const int lane = lane_id();
+    bool taken[4];
+#pragma unroll
+    for (int i = 0; i < 4; ++i) taken[i] = (lane + 64 * i) >= E;
+    float selv[8];
+    int sele[8];
+#pragma unroll
+    for (int j = 0; j < 8; ++j) {
+        if (j >= k) break;
+        float bv = -INFINITY;
+        int be = 0x7fffffff;
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+            const int e = lane + 64 * i;
+            if (!taken[i] && (v[i] > bv || (v[i] == bv && e < be))) {
+                bv = v[i];
+                be = e;
+            }
+        }
+#pragma unroll
+        for (int off = 32; off >= 1; off >>= 1) {
+            const float ov = __shfl_xor(bv, off, 64);
+            const int oe = __shfl_xor(be, off, 64);
+            if (ov > bv || (ov == bv && oe < be)) {
+                bv = ov;
+                be = oe;
+            }
+        }
+#pragma unroll
+        for (int i = 0; i < 4; ++i)
+            if (be == lane + 64 * i) taken[i] = true;
+        selv[j] = bv;
+        sele[j] = be;
+    }
+    const float top = selv[0];
+    float sum = 0.f, mine = 0.f;
+    int mye = 0;
+#pragma unroll
+    for (int j = 0; j < 8; ++j) {
+        if (j >= k) break;
+        const float term = (selv[j] == top) ? 1.0f : expf(selv[j] - top);
+        sum += term;
+        if (j == lane) {
+            mine = term;
+            mye = sele[j];
+        }
+    }
+    if (lane < k) {
+        out_idx[lane] = mye;
+        out_w[lane] = mine / sum;
+        if (lds_idx) lds_idx[lane] = mye;
+    }
+}
+
+// Router scores of tokens [t0, t0 + 16*TT) for all E experts, bf16 inputs, MFMA.
+// The 16 waves of the workgroup are TT token tiles x KP K parts (TT * KP = 16);
+// K part p takes the 32-wide K steps p, p + KP, p + 2 KP, ...  Partial tiles go
+// through `red` ([KP][16 TT][64] fp32) and are added in K-part order, so the
+// fp32 scores do not depend on timing.  Result: s_lg[row][e] = score + bias[e]
+// for row = t - t0 (rows of tokens >= T are left as garbage).
+template <int TT, int KP>
+__device__ void router_scores_bf16(int T, int H, int E, const uint16_t* __restrict__ x,
+                                   const uint16_t* __restrict__ wr, const float* __restrict__ bias, int t0,
+                                   float* s_lg, float* red) {
+    static_assert(TT * KP == kFrontWaves, "16 waves");
+    constexpr int U = 4;
+    const int wave = threadIdx.x >> 6, lane = lane_id();
+    const int r = lane & 15, kq = (lane >> 4) * 8;
+    const int tt = wave % TT, kp = wave / TT;
+    const int tok = t0 + 16 * tt + r;
+    const uint16_t* xp = (tok < T) ? x + (size_t)tok * H + kq : nullptr;
+    const int nsteps = H / 32;
+    const int n_my = (nsteps > kp) ? (nsteps - kp + KP - 1) / KP : 0;
+    for (int c0 = 0; c0 < E; c0 += kScoreChunk) {
+        f32x4 acc[4];
+        const uint16_t* wp[4];
+        bool live[4];
+#pragma unroll
+        for (int m = 0; m < 4; ++m) {
+            acc[m] = f32x4{0.f, 0.f, 0.f, 0.f};
+            const int e = c0 + 16 * m + r;
+            live[m] = c0 + 16 * m < E;
+            wp[m] = (e < E) ? wr + (size_t)e * H + kq : nullptr;
+        }
+        for (int i = 0; i < n_my; i += U) {
+            bf16x8 A[U][4], B[U];
+#pragma unroll
+            for (int u = 0; u < U; ++u) {
+                const int s = kp + KP * (i + u);
+                const bool ok = i + u < n_my;
+                B[u] = (ok && xp) ? load_bf16x8(xp + s * 32) : zero_bf16x8();
+#pragma unroll
+                for (int m = 0; m < 4; ++m) A[u][m] = (ok && wp[m]) ? load_bf16x8(wp[m] + s * 32) : zero_bf16x8();
+            }
+#pragma unroll
+            for (int u = 0; u < U; ++u)
+#pragma unroll
+                for (int m = 0; m < 4; ++m)
+                    if (live[m]) acc[m] = mfma16x16x32(A[u][m], B[u], acc[m]);
+        }
+        // lane holds experts 16m + 4(lane/16) + i of token row 16 tt + r
+#pragma unroll
+        for (int m = 0; m < 4; ++m)
+#pragma unroll
+            for (int i = 0; i < 4; ++i)
+                red[(kp * 16 * TT + 16 * tt + r) * kScoreChunk + 16 * m + 4 * (lane >> 4) + i] = acc[m][i];
+        __syncthreads();
+        for (int idx = threadIdx.x; idx < 16 * TT * kScoreChunk; idx += kFrontThreads) {
+            const int row = idx / kScoreChunk, el = idx % kScoreChunk, e = c0 + el;
+            if (e >= E) continue;
+            float v = red[row * kScoreChunk + el];
+            for (int p = 1; p < KP; ++p) v += red[(p * 16 * TT + row) * kScoreChunk + el];
+            s_lg[row * kLgPitch + e] = v + (bias ? bias[e] : 0.f);
+        }
+        __syncthreads();
+    }
+}
+
+// fp32 inputs: one (token, expert) dot product per thread, plain fp32 FMA.
+__device__ inline void router_scores_f32(int T, int H, int E, const float* __restrict__ x,
+                                         const float* __restrict__ wr, const float* __restrict__ bias, int t0,
+                                         int rows, float* s_lg) {
+    for (int idx = threadIdx.x; idx < rows * E; idx += blockDim.x) {
+        const int row = idx / E, e = idx % E, t = t0 + row;
+        if (t >= T) continue;
+        float acc = 0.f;
+        for (int h = 0; h < H; ++h) acc = fmaf(x[(size_t)t * H + h], wr[(size_t)e * H + h], acc);
+        s_lg[row * kLgPitch + e] = acc + (bias ? bias[e] : 0.f);
+    }
+    __syncthreads();
+}
+
+// LDS ints the repack needs.
+constexpr int kRepackLdsInts = 3 * 256 + kFrontWaves * 256 + 4;
+
+// Expert-aligned repacking of T*k pairs by one 1024-thread workgroup.
+//   1. histogram with LDS atomics (order-free);
+//   2. one wave scans the counts in group order -- resident experts by id, then
+//      offloaded experts by id -- into segment starts and n_res;
+//   3. pairs are scattered in chunks of 1024, one per thread: inside a wave the
+//      lanes holding the same expert are found with 8 ballots over the bits of
+//      the expert id, a lane's rank is the popcount of the matching lanes below
+//      it, and each wave adds the counts of the waves before it (LDS).  Pairs
+//      keep their index order inside an expert: a stable counting sort, no
+//      global atomics.
+// idx may point to global or LDS memory; ids outside [0, E) are dropped
+// (inv_perm = -1).  Ends with a barrier.
+__device__ inline void repack_block(int T, int E, int k, int slots, const int32_t* idx,
+                                    const int32_t* __restrict__ expert_slot, int32_t* __restrict__ counts,
+                                    int32_t* __restrict__ seg_start, int32_t* __restrict__ perm,
+                                    int32_t* __restrict__ inv_perm, int32_t* __restrict__ n_res, int* lds) {
+    int* s_cnt = lds;
+    int* s_base = lds + 256;
+    int* s_res = lds + 512;
+    int* s_wcnt = lds + 768;                // [16][256]
+    int* s_nres = lds + 768 + kFrontWaves * 256;
+    const int tid = threadIdx.x, wave = tid >> 6, lane = lane_id();
+    const int P = T * k;
+
+    for (int e = tid; e < 256; e += kFrontThreads) {
+        s_cnt[e] = 0;
+        s_res[e] = (e < E) ? (is_resident(expert_slot[e], slots) ? 1 : 0) : 0;
+    }
+    __syncthreads();
+    for (int q = tid; q < P; q += kFrontThreads) {
+        const int e = idx[q];
+        if (e >= 0 && e < E) atomicAdd(&s_cnt[e], 1);
+    }
+    __syncthreads();
+    if (wave == 0) {
+        int rs = 0, os = 0;  // lane owns experts 4 lane .. 4 lane + 3
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+            const int e = 4 * lane + i;
+            if (e < E) {
+                if (s_res[e]) rs += s_cnt[e];
+                else os += s_cnt[e];
+            }
+        }
+        int rinc = rs, oinc = os;
+#pragma unroll
+        for (int off = 1; off < 64; off <<= 1) {
+            const int a = __shfl_up(rinc, off, 64);
+            const int b = __shfl_up(oinc, off, 64);
+            if (lane >= off) {
+                rinc += a;
+                oinc += b;
+            }
+        }
+        const int rtot = __shfl(rinc, 63, 64);
+        int rp = rinc - rs, op = rtot + (oinc - os);
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+            const int e = 4 * lane + i;
+            if (e < E) {
+                if (s_res[e]) {
+                    s_base[e] = rp;
+                    rp += s_cnt[e];
+                } else {
+                    s_base[e] = op;
+                    op += s_cnt[e];
+                }
+            }
+        }
+        if (lane == 0) *s_nres = rtot;
+    }
+    __syncthreads();
+    for (int e = tid; e < E; e += kFrontThreads) {
+        counts[e] = s_cnt[e];
+        seg_start[e] = s_base[e];
+    }
+    if (tid == 0) *n_res = *s_nres;
+
+    const unsigned long long lt_mask = (1ull << lane) - 1ull;
+    for (int c0 = 0; c0 < P; c0 += kFrontThreads) {
+        for (int i = tid; i < kFrontWaves * 256; i += kFrontThreads) s_wcnt[i] = 0;
+        __syncthreads();
+        const int q = c0 + tid;
+        const int e = (q < P) ? idx[q] : -1;
+        const bool valid = (e >= 0 && e < E);
+        unsigned long long m = __ballot(valid);
+#pragma unroll
+        for (int b = 0; b < 8; ++b) {
+            const bool bit = valid && ((e >> b) & 1);
+            const unsigned long long bb = __ballot(bit);
+            m &= bit ? bb : ~bb;
+        }
+        const int rank = __popcll(m & lt_mask);
+        if (valid && rank == 0) s_wcnt[wave * 256 + e] = __popcll(m);
+        __syncthreads();
+        if (valid) {
+            int p = s_base[e] + rank;
+            for (int w = 0; w < wave; ++w) p += s_wcnt[w * 256 + e];
+            perm[p] = q;
+            inv_perm[q] = p;
+        } else if (q < P) {
+            inv_perm[q] = -1;
+        }
+        __syncthreads();
+        for (int ee = tid; ee < E; ee += kFrontThreads) {
+            int sum = 0;
+#pragma unroll
+            for (int w = 0; w < kFrontWaves; ++w) sum += s_wcnt[w * 256 + ee];
+            s_base[ee] += sum;
+        }
+        __syncthreads();
+    }
+}
+
+}  // namespace saem

@@ -15,6 +15,20 @@
 namespace saem {
 namespace {
 
+// sum_c y[c][row, h..h+3] over the ks K chunks, in chunk order; all loads issued first.
+__device__ __forceinline__ f32x4 sum_chunks(const float* __restrict__ y, int ks, long long stride, size_t off) {
+    constexpr int kMax = 16;
+    f32x4 p[kMax];
+#pragma unroll
+    for (int c = 0; c < kMax; ++c)
+        if (c < ks) p[c] = *reinterpret_cast<const f32x4*>(y + c * stride + off);
+    f32x4 v = p[0];
+#pragma unroll
+    for (int c = 1; c < kMax; ++c)
+        if (c < ks) v += p[c];
+    return v;
+}
+
 template <bool kOutBf16>
 __global__ void __launch_bounds__(256)
     k_combine(int T, int H, int E, int k, int S, int slots, const int32_t* __restrict__ topk_idx,
@@ -35,18 +49,14 @@ __global__ void __launch_bounds__(256)
         if (p < 0 || p >= P) continue;
         const float w = topk_w[q];
         if (is_resident(expert_slot[e], slots)) {
-            f32x4 v = *reinterpret_cast<const f32x4*>(y + (size_t)p * H + h);
-            for (int c = 1; c < ks; ++c) v += *reinterpret_cast<const f32x4*>(y + c * stride + (size_t)p * H + h);
-            acc += w * v;
+            acc += w * sum_chunks(y, ks, stride, (size_t)p * H + h);
         } else if (y_off && p >= nres) {
             acc += w * *reinterpret_cast<const f32x4*>(y_off + (size_t)(p - nres) * H + h);
         }
     }
     for (int s = 0; s < S; ++s) {
         const size_t row = (size_t)P + (size_t)s * T + t;
-        f32x4 v = *reinterpret_cast<const f32x4*>(y + row * H + h);
-        for (int c = 1; c < ks; ++c) v += *reinterpret_cast<const f32x4*>(y + c * stride + row * H + h);
-        acc += v;
+        acc += sum_chunks(y, ks, stride, row * H + h);
     }
     if (kOutBf16) {
         u32x2 packed;

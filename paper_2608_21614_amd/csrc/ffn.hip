@@ -55,7 +55,31 @@ struct Args {
     int max_routed;   // routed groups the grid reserves (>= active resident experts)
     int ipg_r;        // items (workgroups) per routed group
     int ipg_s;        // items per shared group
+    // offloaded-row pack done by the workgroups past the FFN items (phase 1 only)
+    const float* topk_w;
+    const int32_t* n_res;
+    void* off_rows;
+    float* off_w;
 };
+
+// off_rows[p - n_res] = x[perm[p] / k] and off_w[p - n_res] = topk_w[perm[p]] for the
+// offloaded rows p = n_res + wg, n_res + wg + nwg, ...
+__device__ void pack_offloaded(const Args& a, int wg, int nwg) {
+    const int P = a.T * a.k;
+    const int nres = *a.n_res;
+    const int chunks = a.H / 8;  // 16-byte chunks of a bf16 row
+    for (int p = nres + wg; p < P; p += nwg) {
+        const int q = a.perm[p];
+        if (q < 0 || q >= P) continue;
+        const int t = q / a.k;
+        if (a.off_rows) {
+            const u32x4* src = reinterpret_cast<const u32x4*>(static_cast<const uint16_t*>(a.x) + (size_t)t * a.H);
+            u32x4* dst = reinterpret_cast<u32x4*>(static_cast<uint16_t*>(a.off_rows) + (size_t)(p - nres) * a.H);
+            for (int c = threadIdx.x; c < chunks; c += blockDim.x) dst[c] = src[c];
+        }
+        if (a.off_w && threadIdx.x == 0) a.off_w[p - nres] = a.topk_w[q];
+    }
+}
 
 // One group of rows: a resident routed expert or a shared expert.
 struct Group {
@@ -141,8 +165,13 @@ __global__ void __launch_bounds__(256) k_ffn_stream(Args a) {
     __shared__ int s_wsum[4];
     __shared__ f32x4 s_red[4][MT][NT][kWave];
 
-    const int nact = list_active(a, s_list, s_wsum);
     const int item = blockIdx.x;
+    const int n_items = a.max_routed * a.ipg_r + a.S * a.ipg_s;
+    if (!kDown && item >= n_items) {  // trailing workgroups pack the offloaded rows
+        pack_offloaded(a, item - n_items, gridDim.x - n_items);
+        return;
+    }
+    const int nact = list_active(a, s_list, s_wsum);
     Group g;
     int sub;
     if (item < a.max_routed * a.ipg_r) {
@@ -581,8 +610,15 @@ __global__ void __launch_bounds__(256) k_reduce_splits(int T, int H, int E, int 
     const int row = blockIdx.x;
     if (row >= rows || (row < P && row >= s_nres)) return;
     for (int h = threadIdx.x * 4; h < H; h += 1024) {
-        f32x4 v = *reinterpret_cast<const f32x4*>(y + (size_t)row * H + h);
-        for (int c = 1; c < ks; ++c) v += *reinterpret_cast<const f32x4*>(y + c * stride + (size_t)row * H + h);
+        constexpr int kMax = 16;  // same order as the combine: chunk 0, then 1, ...
+        f32x4 p[kMax];
+#pragma unroll
+        for (int c = 0; c < kMax; ++c)
+            if (c < ks) p[c] = *reinterpret_cast<const f32x4*>(y + c * stride + (size_t)row * H + h);
+        f32x4 v = p[0];
+#pragma unroll
+        for (int c = 1; c < kMax; ++c)
+            if (c < ks) v += p[c];
         *reinterpret_cast<f32x4*>(y_out + (size_t)row * H + h) = v;
     }
 }
@@ -597,6 +633,8 @@ bool use_stream(const Shape& s) { return s.bf16 && s.T <= 64; }
 
 }  // namespace
 
+bool ffn_packs_offloaded(const Shape& s) { return use_stream(s); }
+
 int ffn_down_splits(const Shape& s) {
     if (!use_stream(s)) return 1;
     // phase-2 work items: (groups) x (H / 64 row tiles) x ks; aim for >= ~2048
@@ -606,7 +644,7 @@ int ffn_down_splits(const Shape& s) {
     int steps = s.F / 32;
     if (s.S > 0 && s.Fs / 32 < steps) steps = s.Fs / 32;
     int ks = 1;
-    while (ks < 16 && (long long)groups * (s.H / 64) * ks < 2048 && steps / (ks * 2) >= 8) ks *= 2;
+    while (ks < 16 && (long long)groups * (s.H / 64) * ks < 2048 && steps / (ks * 2) >= 8) ks *= 2;  // ks <= 16
     return ks;
 }
 
@@ -623,6 +661,10 @@ hipError_t launch_grouped_ffn(const Shape& s, const FfnArgs& fa, hipStream_t st,
     a.w13 = fa.w13; a.w2 = fa.w2; a.ws13 = fa.ws13; a.ws2 = fa.ws2;
     a.act = fa.act; a.Fa = fa.Fa; a.y = fa.y; a.ks = fa.ks; a.y_ks_stride = fa.y_ks_stride;
     a.max_routed = max_routed_groups(s);
+    a.topk_w = fa.topk_w;
+    a.n_res = fa.n_res;
+    a.off_rows = fa.off_rows;
+    a.off_w = fa.off_w;
     if (!s.bf16) {
         a.ipg_r = a.ipg_s = 1;
         const int groups = a.max_routed + s.S;
@@ -639,6 +681,10 @@ hipError_t launch_grouped_ffn(const Shape& s, const FfnArgs& fa, hipStream_t st,
         a.ipg_r = s.F / 32;
         a.ipg_s = s.S > 0 ? s.Fs / 32 : 1;
         int grid = a.max_routed * a.ipg_r + s.S * a.ipg_s;
+        if (fa.off_rows || fa.off_w) {
+            const int P = s.T * s.k;
+            grid += P < 64 ? P : 64;  // pack workgroups (P >= 1 here)
+        }
         if (grid > 0) {
             switch (nt) {
                 case 1: hipLaunchKernelGGL((k_ffn_stream<1, false>), dim3(grid), dim3(256), 0, st, a); break;

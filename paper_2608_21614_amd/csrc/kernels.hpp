@@ -13,9 +13,20 @@ struct Shape {
     int bf16;  // 1: bf16 activations and weights, 0: fp32
 };
 
-// Router scores + top-k gate.
+// Decode batches (T <= 64) route through K-sliced partial scores: the number of
+// slices (0 for larger batches); their scratch is [slices][64][E] fp32.
+bool front_small_fits(const Shape& s);
+int router_slices(const Shape& s);
+
+// Router scores + top-k gate.  part: scratch of router_slices(s) * 64 * E floats.
 hipError_t launch_route_topk(const Shape& s, const void* x, const void* w_router, const float* bias, float* logits,
-                             bool logits_in, int32_t* topk_idx, float* topk_w, hipStream_t st);
+                             bool logits_in, int32_t* topk_idx, float* topk_w, float* part, hipStream_t st);
+
+// Decode front end (T <= 64): scores + top-k + repacking, two launches.
+hipError_t launch_front_small(const Shape& s, const void* x, const void* w_router, const float* bias, float* logits,
+                              bool logits_in, int32_t* topk_idx, float* topk_w, float* part,
+                              const int32_t* expert_slot, int32_t* counts, int32_t* seg_start, int32_t* perm,
+                              int32_t* inv_perm, int32_t* n_res, hipStream_t st);
 
 // Histogram, group-order scan, stable permutation, residency split.
 hipError_t launch_repack(const Shape& s, const int32_t* topk_idx, const int32_t* expert_slot, int32_t* counts,
@@ -41,7 +52,15 @@ struct FfnArgs {
     float* y;           // [ks][rows][H] fp32 partial sums over K chunks of the down projection
     int ks;             // number of K chunks of the down projection
     long long y_ks_stride;
+    // optional: pack the offloaded rows in extra workgroups of phase 1 (decode path only)
+    const float* topk_w = nullptr;
+    const int32_t* n_res = nullptr;
+    void* off_rows = nullptr;
+    float* off_w = nullptr;
 };
+
+// True when the FFN can fold the offloaded-row pack into its phase-1 launch.
+bool ffn_packs_offloaded(const Shape& s);
 
 // Number of K chunks the down projection is split into (1 = direct sums).
 int ffn_down_splits(const Shape& s);

@@ -113,11 +113,13 @@ def test_invalid_pointers_rejected_before_any_launch(pkg):
     d = ctypes.byref(pkg.make_dims(**GOOD))
     f = _fake()
     # route: NULL outputs
-    assert lib.moe_route_topk(d, f, f, None, None, 0, f, f, None) == 1
+    assert lib.moe_route_topk(d, f, f, None, None, 0, f, f, f, 1 << 40, None) == 1
     # route: misaligned x
-    assert lib.moe_route_topk(d, _fake(0x10004), f, None, f, 0, f, f, None) == 1
+    assert lib.moe_route_topk(d, _fake(0x10004), f, None, f, 0, f, f, f, 1 << 40, None) == 1
     # route: unknown flag
-    assert lib.moe_route_topk(d, f, f, None, f, 4, f, f, None) == 1
+    assert lib.moe_route_topk(d, f, f, None, f, 4, f, f, f, 1 << 40, None) == 1
+    # route: workspace too small
+    assert lib.moe_route_topk(d, f, f, None, f, 0, f, f, f, 16, None) == 3
     # repack: off_rows requested without x
     assert lib.moe_repack(d, f, f, f, None, f, f, f, f, f, f, None, None) == 1
     # combine: bad out dtype, y_off without n_res

@@ -102,7 +102,8 @@ def test_route_topk_given_scores_bit_exact(moe, T, E, k):
     d_lg = _dev(lg)
     d_idx = torch.empty((T, k), dtype=torch.int32, device="cuda")
     d_w = torch.empty((T, k), dtype=torch.float32, device="cuda")
-    moe.moe_route_topk(dims, None, None, None, d_lg, d_idx, d_w, logits_in=True)
+    ws = torch.empty(moe.moe_workspace_bytes(dims), dtype=torch.uint8, device="cuda")
+    moe.moe_route_topk(dims, None, None, None, d_lg, d_idx, d_w, ws, logits_in=True)
     torch.cuda.synchronize()
     ref_idx, ref_w = oracle.topk(lg.astype(np.float64), k)
     np.testing.assert_array_equal(_host(d_idx), ref_idx)
@@ -126,8 +127,9 @@ def test_route_topk_computed_scores(moe, dtype, T, H, E, k, bias):
     d_lg = torch.empty((T, E), dtype=torch.float32, device="cuda")
     d_idx = torch.empty((T, k), dtype=torch.int32, device="cuda")
     d_w = torch.empty((T, k), dtype=torch.float32, device="cuda")
+    ws = torch.empty(moe.moe_workspace_bytes(dims), dtype=torch.uint8, device="cuda")
     moe.moe_route_topk(dims, _dev(lay.x), _dev(lay.w_router), None if lay.bias is None else _dev(lay.bias),
-                       d_lg, d_idx, d_w)
+                       d_lg, d_idx, d_w, ws)
     torch.cuda.synchronize()
     lg_ref = oracle.router_logits(lay.x, lay.w_router, lay.bias)
     lg = _host(d_lg).astype(np.float64)
@@ -200,7 +202,8 @@ def test_offload_pack_bit_exact(moe):
     d_lg = torch.empty((T, E), dtype=torch.float32, device="cuda")
     d_idx = torch.empty((T, k), dtype=torch.int32, device="cuda")
     d_w = torch.empty((T, k), dtype=torch.float32, device="cuda")
-    moe.moe_route_topk(dims, _dev(lay.x), _dev(lay.w_router), _dev(lay.bias), d_lg, d_idx, d_w)
+    ws = torch.empty(moe.moe_workspace_bytes(dims), dtype=torch.uint8, device="cuda")
+    moe.moe_route_topk(dims, _dev(lay.x), _dev(lay.w_router), _dev(lay.bias), d_lg, d_idx, d_w, ws)
     counts = torch.empty(E, dtype=torch.int32, device="cuda")
     seg = torch.empty(E, dtype=torch.int32, device="cuda")
     perm = torch.empty(T * k, dtype=torch.int32, device="cuda")
@@ -333,7 +336,7 @@ def _standalone_chain(moe, dev, y_off=None):
     c = dev.cfg
     T, E, k, H, S = c.tokens, c.experts, c.top_k, c.hidden, c.shared
     o = dev.alloc_outputs()
-    moe.moe_route_topk(dev.dims, dev.x, dev.w_router, dev.bias, o["logits"], o["topk_idx"], o["topk_w"])
+    moe.moe_route_topk(dev.dims, dev.x, dev.w_router, dev.bias, o["logits"], o["topk_idx"], o["topk_w"], dev.ws)
     moe.moe_repack(dev.dims, o["topk_idx"], o["topk_w"], dev.expert_slot, dev.x, o["counts"], o["seg_start"],
                    o["perm"], o["inv_perm"], o["n_res"], o["off_rows"], o["off_w"])
     y = torch.zeros((T * k + S * T, H), dtype=torch.float32, device="cuda")
