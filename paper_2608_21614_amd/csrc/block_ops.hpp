@@ -1,5 +1,5 @@
 // block_ops.hpp -- workgroup-level building blocks of the routing front end:
-// router scores on MFMA, the wave-wide top-k gate, and the single-workgroup
+// router scores on MFMA, the rank-based top-k gate, and the single-workgroup
 // counting sort that repacks the (token, expert) pairs.
 #pragma once
 
@@ -14,63 +14,54 @@ constexpr int kFrontWaves = kFrontThreads / kWave;
 constexpr int kLgPitch = 257;                   // LDS row pitch of a score tile (E <= 256)
 constexpr int kScoreChunk = 64;                 // experts (4 MFMA row tiles) per reduction pass
 
-// Top-k of one token's scores held as v[i] = score of expert lane + 64 i (one wave).
-// Selection order: higher score first, equal scores -> lower expert id.  Writes
-// out_idx[0..k), out_w[0..k) (softmax over the selected scores) and, if given,
-// lds_idx[0..k).
-__device__ inline void topk_wave(const float (&v)[4], int E, int k, int32_t* out_idx, float* out_w, int32_t* lds_idx) {
-    const int lane = lane_id();
-    bool taken[4];
-#pragma unroll
-    for (int i = 0; i < 4; ++i) taken[i] = (lane + 64 * i) >= E;
-    float selv[8];
-    int sele[8];
-#pragma unroll
-    for (int j = 0; j < 8; ++j) {
-        if (j >= k) break;
-        float bv = -INFINITY;
-        int be = 0x7fffffff;
-#pragma unroll
-        for (int i = 0; i < 4; ++i) {
-            const int e = lane + 64 * i;
-            if (!taken[i] && (v[i] > bv || (v[i] == bv && e < be))) {
-                bv = v[i];
-                be = e;
-            }
+// LDS the top-k needs: selected (score, expert) of up to 64 rows x 8.
+constexpr int kTopkLdsWords = 2 * 64 * 8;
+
+// Top-k gate of `rows` tokens whose scores sit in LDS (s_lg, pitch kLgPitch),
+// by the whole workgroup.  Experts are totally ordered by (score desc, expert
+// id asc); the rank of expert e in row t is the number of experts before it in
+// that order, computed for every (t, e) in parallel, and e is the j-th choice
+// of t iff its rank is j < k.  The gate of choice j is exp(s_j - s_0) /
+// sum_j' exp(s_j' - s_0), summed in j order; a score equal to the top one
+// contributes exactly 1 (so all-equal rows, -inf included, get 1/k).
+// Writes out_idx/out_w rows [t0, t0 + rows) and, if given, lds_idx[t*k + j].
+// Ends with a barrier.  (NaN scores: undefined selection, never an index
+// outside [-1, E).)
+__device__ inline void topk_rank_block(const float* s_lg, int rows, int E, int k, int t0, int32_t* out_idx,
+                                       float* out_w, int32_t* lds_idx, float* s_selv, int* s_sele) {
+    for (int i = threadIdx.x; i < rows * 8; i += blockDim.x) s_sele[i] = -1;
+    __syncthreads();
+    for (int idx = threadIdx.x; idx < rows * E; idx += blockDim.x) {
+        const int t = idx / E, e = idx % E;
+        const float* row = s_lg + t * kLgPitch;
+        const float v = row[e];
+        int rank = 0;
+        for (int e2 = 0; e2 < E; ++e2) {
+            const float v2 = row[e2];
+            rank += (v2 > v || (v2 == v && e2 < e)) ? 1 : 0;
         }
-#pragma unroll
-        for (int off = 32; off >= 1; off >>= 1) {
-            const float ov = __shfl_xor(bv, off, 64);
-            const int oe = __shfl_xor(be, off, 64);
-            if (ov > bv || (ov == bv && oe < be)) {
-                bv = ov;
-                be = oe;
-            }
-        }
-#pragma unroll
-        for (int i = 0; i < 4; ++i)
-            if (be == lane + 64 * i) taken[i] = true;
-        selv[j] = bv;
-        sele[j] = be;
-    }
-    const float top = selv[0];
-    float sum = 0.f, mine = 0.f;
-    int mye = 0;
-#pragma unroll
-    for (int j = 0; j < 8; ++j) {
-        if (j >= k) break;
-        const float term = (selv[j] == top) ? 1.0f : expf(selv[j] - top);
-        sum += term;
-        if (j == lane) {
-            mine = term;
-            mye = sele[j];
+        if (rank < k) {
+            s_selv[t * 8 + rank] = v;
+            s_sele[t * 8 + rank] = e;
         }
     }
-    if (lane < k) {
-        out_idx[lane] = mye;
-        out_w[lane] = mine / sum;
-        if (lds_idx) lds_idx[lane] = mye;
+    __syncthreads();
+    for (int idx = threadIdx.x; idx < rows * k; idx += blockDim.x) {
+        const int t = idx / k, j = idx % k;
+        const float top = s_selv[t * 8];
+        float sum = 0.f, mine = 0.f;
+        for (int jj = 0; jj < k; ++jj) {
+            const float sv = s_selv[t * 8 + jj];
+            const float term = (sv == top) ? 1.0f : expf(sv - top);
+            sum += term;
+            if (jj == j) mine = term;
+        }
+        const int e = s_sele[t * 8 + j];
+        out_idx[(size_t)(t0 + t) * k + j] = e;
+        out_w[(size_t)(t0 + t) * k + j] = mine / sum;
+        if (lds_idx) lds_idx[t * k + j] = e;
     }
+    __syncthreads();
 }
 
 // Router scores of tokens [t0, t0 + 16*TT) for all E experts, bf16 inputs, MFMA.

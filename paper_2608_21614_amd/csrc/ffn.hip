@@ -254,13 +254,13 @@ __global__ void __launch_bounds__(256) k_ffn_stream(Args a) {
         }
     };
     auto mma = [&](const bf16x8 (&A)[U][MT], const bf16x8 (&B)[U][NT]) {
+        // tiles past the group's last token see zero operands: no branch, fewer live registers
 #pragma unroll
         for (int u = 0; u < U; ++u)
 #pragma unroll
             for (int j = 0; j < NT; ++j)
-                if (j < ntile)
 #pragma unroll
-                    for (int m = 0; m < MT; ++m) acc[m][j] = mfma16x16x32(A[u][m], B[u][j], acc[m][j]);
+                for (int m = 0; m < MT; ++m) acc[m][j] = mfma16x16x32(A[u][m], B[u][j], acc[m][j]);
     };
     const int nb = n_my / U;
     {
@@ -282,9 +282,8 @@ __global__ void __launch_bounds__(256) k_ffn_stream(Args a) {
         for (int j = 0; j < NT; ++j) B[j] = (j < ntile && bp[j]) ? load_bf16x8(bp[j] + s * 32) : zero_bf16x8();
 #pragma unroll
         for (int j = 0; j < NT; ++j)
-            if (j < ntile)
 #pragma unroll
-                for (int m = 0; m < MT; ++m) acc[m][j] = mfma16x16x32(A[m], B[j], acc[m][j]);
+            for (int m = 0; m < MT; ++m) acc[m][j] = mfma16x16x32(A[m], B[j], acc[m][j]);
     }
 
 #pragma unroll
@@ -644,7 +643,7 @@ int ffn_down_splits(const Shape& s) {
     int steps = s.F / 32;
     if (s.S > 0 && s.Fs / 32 < steps) steps = s.Fs / 32;
     int ks = 1;
-    while (ks < 16 && (long long)groups * (s.H / 64) * ks < 2048 && steps / (ks * 2) >= 8) ks *= 2;  // ks <= 16
+    while (ks < 16 && (long long)groups * (s.H / 64) * ks < 2048 && steps / (ks * 2) >= 16) ks *= 2;  // ks <= 16
     return ks;
 }
 

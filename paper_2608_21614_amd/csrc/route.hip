@@ -2,10 +2,11 @@
 // a router), and the decode front end (scores + top-k + repacking).
 //
 // Scores run on MFMA (v_mfma_f32_16x16x32_bf16): router rows are the M side,
-// 16 tokens the N side.  The top-k runs one wave per token (block_ops.hpp).
+// 16 tokens the N side.
 //
 //  * T > 64 (prefill): k_route_topk, 16 tokens per 1024-thread workgroup whose
 //    16 waves split K and add their partial tiles in a fixed order.
+// The top-k ranks every (token, expert) in parallel (topk_rank_block).
 //  * T <= 64 (decode): k_router_partial spreads the scores over one workgroup
 //    per K slice (a single CU cannot stream the batch and the router fast
 //    enough), then k_front_small adds the slices in order and runs the top-k
@@ -25,8 +26,9 @@ __global__ void __launch_bounds__(kFrontThreads)
                  int32_t* __restrict__ topk_idx, float* __restrict__ topk_w) {
     __shared__ float s_lg[16 * kLgPitch];
     __shared__ float s_red[kFrontWaves * 16 * kScoreChunk];
+    __shared__ float s_selv[64 * 8];
+    __shared__ int s_sele[64 * 8];
     const int t0 = blockIdx.x * 16;
-    const int wave = threadIdx.x >> 6, lane = lane_id();
     if (!logits_in) {
         if (kBf16)
             router_scores_bf16<1, kFrontWaves>(T, H, E, static_cast<const uint16_t*>(x),
@@ -35,23 +37,15 @@ __global__ void __launch_bounds__(kFrontThreads)
             router_scores_f32(T, H, E, static_cast<const float*>(x), static_cast<const float*>(wr), bias, t0, 16,
                               s_lg);
     }
-    const int t = t0 + wave;  // 16 waves, 16 tokens
-    if (t >= T) return;
-    float v[4];
-#pragma unroll
-    for (int i = 0; i < 4; ++i) {
-        const int e = lane + 64 * i;
-        v[i] = -INFINITY;
-        if (e < E) {
-            if (logits_in) {
-                v[i] = logits[(size_t)t * E + e];
-            } else {
-                v[i] = s_lg[wave * kLgPitch + e];
-                logits[(size_t)t * E + e] = v[i];
-            }
-        }
+    const int rows = min(16, T - t0);
+    // scores <-> global, coalesced
+    for (int idx = threadIdx.x; idx < rows * E; idx += kFrontThreads) {
+        const int row = idx / E, e = idx % E;
+        if (logits_in) s_lg[row * kLgPitch + e] = logits[(size_t)(t0 + row) * E + e];
+        else logits[(size_t)(t0 + row) * E + e] = s_lg[row * kLgPitch + e];
     }
-    topk_wave(v, E, k, topk_idx + (size_t)t * k, topk_w + (size_t)t * k, nullptr);
+    __syncthreads();
+    topk_rank_block(s_lg, rows, E, k, t0, topk_idx, topk_w, nullptr, s_selv, s_sele);
 }
 
 // Decode batches: part[slice][t][e] = sum over the slice's K steps of x[t] . w_router[e].
@@ -128,43 +122,47 @@ __global__ void __launch_bounds__(kFrontThreads)
     __shared__ float s_lg[64 * kLgPitch];
     __shared__ int s_rep[kRepackLdsInts];
     __shared__ int32_t s_idx[64 * 8];
-    const int wave = threadIdx.x >> 6, lane = lane_id();
+    __shared__ float s_selv[64 * 8];
+    __shared__ int s_sele[64 * 8];
     if (!logits_in) {
-        for (int idx = threadIdx.x; idx < T * E; idx += kFrontThreads) {
-            const int t = idx / E, e = idx % E;
-            // issue the loads of 16 slices at once, then add them in slice order
-            float v = 0.f;
+        // add the K-sliced partials in slice order (+ bias); 4 entries x 16 slices of loads in flight per thread
+        constexpr int kPer = 4;
+        for (int base = threadIdx.x; base < T * E; base += kPer * kFrontThreads) {
+            float v[kPer];
+#pragma unroll
+            for (int i = 0; i < kPer; ++i) v[i] = 0.f;
             for (int b = 0; b < nsl; b += 16) {
-                float p[16];
+                float p[kPer][16];
 #pragma unroll
-                for (int j = 0; j < 16; ++j) p[j] = (b + j < nsl) ? part[(size_t)(b + j) * 64 * E + idx] : 0.f;
+                for (int i = 0; i < kPer; ++i) {
+                    const int idx = base + i * kFrontThreads;
 #pragma unroll
-                for (int j = 0; j < 16; ++j)
-                    if (b + j < nsl) v = (b + j == 0) ? p[j] : v + p[j];
+                    for (int j = 0; j < 16; ++j)
+                        p[i][j] = (idx < T * E && b + j < nsl) ? part[(size_t)(b + j) * 64 * E + idx] : 0.f;
+                }
+#pragma unroll
+                for (int i = 0; i < kPer; ++i)
+#pragma unroll
+                    for (int j = 0; j < 16; ++j)
+                        if (b + j < nsl) v[i] = (b + j == 0) ? p[i][j] : v[i] + p[i][j];
             }
-            s_lg[t * kLgPitch + e] = v + (bias ? bias[e] : 0.f);
-        }
-        __syncthreads();
-    }
-    for (int t = wave; t < T; t += kFrontWaves) {
-        float v[4];
 #pragma unroll
-        for (int i = 0; i < 4; ++i) {
-            const int e = lane + 64 * i;
-            v[i] = -INFINITY;
-            if (e < E) {
-                if (logits_in) {
-                    v[i] = logits[(size_t)t * E + e];
-                } else {
-                    v[i] = s_lg[t * kLgPitch + e];
-                    logits[(size_t)t * E + e] = v[i];
+            for (int i = 0; i < kPer; ++i) {
+                const int idx = base + i * kFrontThreads;
+                if (idx < T * E) {
+                    const int t = idx / E, e = idx % E;
+                    const float sc = v[i] + (bias ? bias[e] : 0.f);
+                    s_lg[t * kLgPitch + e] = sc;
+                    logits[idx] = sc;
                 }
             }
         }
-        topk_wave(v, E, k, topk_idx + (size_t)t * k, topk_w + (size_t)t * k, s_idx + t * k);
+    } else {
+        for (int idx = threadIdx.x; idx < T * E; idx += kFrontThreads) s_lg[(idx / E) * kLgPitch + idx % E] = logits[idx];
     }
-    if (!repack) return;
     __syncthreads();
+    topk_rank_block(s_lg, T, E, k, 0, topk_idx, topk_w, s_idx, s_selv, s_sele);
+    if (!repack) return;
     repack_block(T, E, k, slots, s_idx, expert_slot, counts, seg_start, perm, inv_perm, n_res, s_rep);
 }
 

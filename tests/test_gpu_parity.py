@@ -297,6 +297,8 @@ EDGE = [
     (33, 128, 256, 64, 8, 0, 0, "bf16", 100),
     (20, 64, 128, 128, 8, 1, 64, "f32", 64),
     (9, 64, 4, 64, 4, 2, 128, "f32", 0),
+    (100, 64, 8, 128, 2, 1, 64, "f32", 4),
+    (2, 4096, 8, 14336, 2, 0, 0, "bf16", 4),
 ]
 
 
