@@ -26,7 +26,9 @@
  *   - Kernel faults surface at the caller's next synchronisation, as usual for
  *     HIP; launch failures return MOE_ERR_HIP.
  *   - Calls on distinct streams with distinct workspaces may run concurrently.
- *   - Every tensor pointer must be 16-byte aligned (MOE_ERR_INVALID_ARG otherwise).
+ *   - Alignment (MOE_ERR_INVALID_ARG otherwise): activations, weights, outputs,
+ *     y, y_off, off_rows and the workspace 16 bytes; index, count, slot, score
+ *     and gate arrays 4 bytes; the int64 stage log 8 bytes.
  *   - Layouts:
  *       x          [T, H]        activations (dims.dtype), row-major
  *       w_router   [E, H]        row e scores expert e (dims.dtype), row-major

@@ -335,3 +335,45 @@ def cache_hit_ratio(counts: np.ndarray, resident: np.ndarray) -> float:
     r = np.asarray(resident, dtype=bool)
     tot = int(c.sum())
     return float((c * r).sum()) / tot if tot else 1.0
+
+
+def stage_replay(counts: np.ndarray, stage_len: np.ndarray, initial_slot: np.ndarray, n_slots: int):
+    """Stage-aware residency over a decode trace (Sections IV-B.2, IV-C.2, V-C).
+
+    counts[step, layer, e]: routed pairs per expert of each (step, layer) call;
+    routing does not depend on where experts live, so the counts are fixed
+    before the policy runs.  A stage's activation log is the sum of its counts
+    over all queries in the batch (Section IV-B.2).
+
+    Online policy (the method): stage s runs with the residency planned from the
+    log of stage s-1 (the first stage with ``initial_slot``).  Clairvoyant policy
+    (the prediction oracle of Section V-C): stage s runs with the residency
+    planned from its own log.  CHR = resident pairs / all pairs; eta_CHR is their
+    ratio (Eq. upper_bound).
+
+    Returns slot_history [n_stages, layers, E] (the slots in effect during each
+    stage), resident [steps, layers, E], chr_online, chr_clairvoyant, eta_chr.
+    """
+    c = np.asarray(counts, dtype=np.int64)
+    steps, layers, E = c.shape
+    ends = np.cumsum(stage_len)
+    starts = ends - stage_len
+    slot = np.asarray(initial_slot, dtype=np.int32).copy()
+    hist = np.empty((len(stage_len), layers, E), dtype=np.int32)
+    resident = np.empty((steps, layers, E), dtype=bool)
+    hit_on = hit_cv = 0
+    for s, (a, b) in enumerate(zip(starts, ends)):
+        hist[s] = slot
+        res = (slot >= 0) & (slot < n_slots)
+        resident[a:b] = res[None]
+        log = c[a:b].sum(axis=0)                     # [layers, E]
+        hit_on += int((log * res).sum())
+        for l in range(layers):
+            own = stage_plan(log[l], n_slots, np.full(E, -1, np.int32))
+            hit_cv += int(log[l][(own >= 0)].sum())
+        slot = np.stack([stage_plan(log[l], n_slots, slot[l]) for l in range(layers)])
+    total = int(c.sum())
+    chr_on = hit_on / total if total else 1.0
+    chr_cv = hit_cv / total if total else 1.0
+    return {"slot_history": hist, "resident": resident, "chr_online": chr_on, "chr_clairvoyant": chr_cv,
+            "eta_chr": chr_on / chr_cv if chr_cv else 1.0}

@@ -14,11 +14,19 @@ using saem::Shape;
 
 constexpr long long kMaxRows = 1ll << 24;  // T*k + S*T rows handled by one call
 
+// Arrays read or written with 16-byte vector accesses (activations, weights,
+// outputs, workspace) must be 16-byte aligned; index, count and gate arrays only
+// need their element alignment (4 bytes; 8 for the int64 stage log).
 bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
+bool aligned4(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 3u) == 0; }
 bool ok_ptr(const void* p) { return p != nullptr && aligned16(p); }
 bool ok_opt(const void* p) { return p == nullptr || aligned16(p); }
-// A required array: non-NULL and aligned, except that an array with no elements may be NULL.
+// A required vector array: non-NULL and aligned, except that an array with no elements may be NULL.
 bool ok_arr(const void* p, long long n) { return n == 0 ? aligned16(p) : ok_ptr(p); }
+// The same for 4-byte element arrays.
+bool ok_ptr4(const void* p) { return p != nullptr && aligned4(p); }
+bool ok_opt4(const void* p) { return p == nullptr || aligned4(p); }
+bool ok_arr4(const void* p, long long n) { return n == 0 ? aligned4(p) : ok_ptr4(p); }
 
 moe_status check_dims(const moe_dims* d) {
     if (!d) return MOE_ERR_INVALID_ARG;
@@ -130,8 +138,8 @@ moe_status moe_route_topk(const moe_dims* dims, const void* x, const void* w_rou
     if (flags & ~MOE_LOGITS_IN) return MOE_ERR_INVALID_ARG;
     const bool lin = (flags & MOE_LOGITS_IN) != 0;
     const long long T = dims->tokens;
-    if (!ok_arr(logits, T) || !ok_arr(topk_idx, T) || !ok_arr(topk_w, T)) return MOE_ERR_INVALID_ARG;
-    if (!lin && (!ok_arr(x, T) || !ok_ptr(w_router) || !ok_opt(bias))) return MOE_ERR_INVALID_ARG;
+    if (!ok_arr4(logits, T) || !ok_arr4(topk_idx, T) || !ok_arr4(topk_w, T)) return MOE_ERR_INVALID_ARG;
+    if (!lin && (!ok_arr(x, T) || !ok_ptr(w_router) || !ok_opt4(bias))) return MOE_ERR_INVALID_ARG;
     const Shape s = shape_of(dims);
     const Layout L = layout_of(s);
     if (!ws || ws_bytes < L.total || !aligned16(ws)) return MOE_ERR_WORKSPACE;
@@ -146,11 +154,11 @@ moe_status moe_repack(const moe_dims* dims, const int32_t* topk_idx, const float
     moe_status st = check_dims(dims);
     if (st != MOE_OK) return st;
     const long long T = dims->tokens;
-    if (!ok_arr(topk_idx, T) || !ok_ptr(expert_slot) || !ok_ptr(counts) || !ok_ptr(seg_start) || !ok_arr(perm, T) ||
-        !ok_arr(inv_perm, T) || !ok_ptr(n_res) || !ok_opt(off_rows) || !ok_opt(off_w))
+    if (!ok_arr4(topk_idx, T) || !ok_ptr4(expert_slot) || !ok_ptr4(counts) || !ok_ptr4(seg_start) ||
+        !ok_arr4(perm, T) || !ok_arr4(inv_perm, T) || !ok_ptr4(n_res) || !ok_opt(off_rows) || !ok_opt4(off_w))
         return MOE_ERR_INVALID_ARG;
     if (off_rows && !ok_arr(x, T)) return MOE_ERR_INVALID_ARG;
-    if (off_w && !ok_arr(topk_w, T)) return MOE_ERR_INVALID_ARG;
+    if (off_w && !ok_arr4(topk_w, T)) return MOE_ERR_INVALID_ARG;
     const Shape s = shape_of(dims);
     hipStream_t hs = static_cast<hipStream_t>(stream);
     hipError_t e = saem::launch_repack(s, topk_idx, expert_slot, counts, seg_start, perm, inv_perm, n_res, hs);
@@ -164,7 +172,7 @@ moe_status moe_grouped_ffn(const moe_dims* dims, const void* x, const int32_t* p
     moe_status st = check_dims(dims);
     if (st != MOE_OK) return st;
     const long long T = dims->tokens;
-    if (!ok_arr(x, T) || !ok_arr(perm, T) || !ok_ptr(counts) || !ok_ptr(seg_start) || !ok_ptr(expert_slot) ||
+    if (!ok_arr(x, T) || !ok_arr4(perm, T) || !ok_ptr4(counts) || !ok_ptr4(seg_start) || !ok_ptr4(expert_slot) ||
         !ok_arr(y, T))
         return MOE_ERR_INVALID_ARG;
     if (dims->slots > 0 && (!ok_ptr(w13) || !ok_ptr(w2))) return MOE_ERR_INVALID_ARG;
@@ -194,10 +202,10 @@ moe_status moe_combine(const moe_dims* dims, const int32_t* topk_idx, const floa
     if (st != MOE_OK) return st;
     if (out_dtype != MOE_F32 && out_dtype != MOE_BF16) return MOE_ERR_INVALID_ARG;
     const long long T = dims->tokens;
-    if (!ok_arr(topk_idx, T) || !ok_arr(topk_w, T) || !ok_arr(inv_perm, T) || !ok_ptr(expert_slot) ||
+    if (!ok_arr4(topk_idx, T) || !ok_arr4(topk_w, T) || !ok_arr4(inv_perm, T) || !ok_ptr4(expert_slot) ||
         !ok_arr(y, T) || !ok_arr(out, T) || !ok_opt(y_off))
         return MOE_ERR_INVALID_ARG;
-    if (y_off && !ok_ptr(n_res)) return MOE_ERR_INVALID_ARG;
+    if (y_off && !ok_ptr4(n_res)) return MOE_ERR_INVALID_ARG;
     const Shape s = shape_of(dims);
     return hip_status(saem::launch_combine(s, topk_idx, topk_w, inv_perm, expert_slot, y, 1, 0, y_off, n_res, out,
                                            out_dtype == MOE_BF16, static_cast<hipStream_t>(stream)));
@@ -212,14 +220,14 @@ moe_status moe_layer_forward(const moe_layer_args* a, void* ws, size_t ws_bytes,
     if (a->out_dtype != MOE_F32 && a->out_dtype != MOE_BF16) return MOE_ERR_INVALID_ARG;
     const bool lin = (a->flags & MOE_LOGITS_IN) != 0;
     const long long T = d->tokens;
-    if (!ok_arr(a->x, T) || !ok_ptr(a->expert_slot) || !ok_arr(a->out, T)) return MOE_ERR_INVALID_ARG;
-    if (!lin && (!ok_ptr(a->w_router) || !ok_opt(a->bias))) return MOE_ERR_INVALID_ARG;
-    if (lin && !ok_arr(a->logits, T)) return MOE_ERR_INVALID_ARG;
+    if (!ok_arr(a->x, T) || !ok_ptr4(a->expert_slot) || !ok_arr(a->out, T)) return MOE_ERR_INVALID_ARG;
+    if (!lin && (!ok_ptr(a->w_router) || !ok_opt4(a->bias))) return MOE_ERR_INVALID_ARG;
+    if (lin && !ok_arr4(a->logits, T)) return MOE_ERR_INVALID_ARG;
     if (d->slots > 0 && (!ok_ptr(a->w13) || !ok_ptr(a->w2))) return MOE_ERR_INVALID_ARG;
     if (d->shared > 0 && (!ok_ptr(a->ws13) || !ok_ptr(a->ws2))) return MOE_ERR_INVALID_ARG;
-    if (!ok_opt(a->logits) || !ok_opt(a->topk_idx) || !ok_opt(a->topk_w) || !ok_opt(a->counts) ||
-        !ok_opt(a->seg_start) || !ok_opt(a->perm) || !ok_opt(a->inv_perm) || !ok_opt(a->n_res) ||
-        !ok_opt(a->off_rows) || !ok_opt(a->off_w))
+    if (!ok_opt4(a->logits) || !ok_opt4(a->topk_idx) || !ok_opt4(a->topk_w) || !ok_opt4(a->counts) ||
+        !ok_opt4(a->seg_start) || !ok_opt4(a->perm) || !ok_opt4(a->inv_perm) || !ok_opt4(a->n_res) ||
+        !ok_opt(a->off_rows) || !ok_opt4(a->off_w))
         return MOE_ERR_INVALID_ARG;
     const Shape s = shape_of(d);
     const Layout L = layout_of(s);
@@ -300,7 +308,8 @@ moe_status moe_pack_weights(const void* src, void* dst, int64_t rows, int64_t co
 }
 
 moe_status moe_stage_accumulate(int32_t experts, const int32_t* counts, int64_t* log, void* stream) {
-    if (experts <= 0 || experts > 256 || !ok_ptr(counts) || !ok_ptr(log)) return MOE_ERR_INVALID_ARG;
+    if (experts <= 0 || experts > 256 || !ok_ptr4(counts) || !log || (reinterpret_cast<uintptr_t>(log) & 7u))
+        return MOE_ERR_INVALID_ARG;
     return hip_status(saem::launch_stage_accumulate(experts, counts, log, static_cast<hipStream_t>(stream)));
 }
 

@@ -114,8 +114,9 @@ def test_invalid_pointers_rejected_before_any_launch(pkg):
     f = _fake()
     # route: NULL outputs
     assert lib.moe_route_topk(d, f, f, None, None, 0, f, f, f, 1 << 40, None) == 1
-    # route: misaligned x
+    # route: misaligned x (activations need 16 bytes), misaligned index array (needs 4)
     assert lib.moe_route_topk(d, _fake(0x10004), f, None, f, 0, f, f, f, 1 << 40, None) == 1
+    assert lib.moe_route_topk(d, f, f, None, f, 0, _fake(0x10002), f, f, 1 << 40, None) == 1
     # route: unknown flag
     assert lib.moe_route_topk(d, f, f, None, f, 4, f, f, f, 1 << 40, None) == 1
     # route: workspace too small

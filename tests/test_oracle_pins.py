@@ -440,3 +440,25 @@ def test_generator_is_deterministic_and_thread_independent(monkeypatch):
     assert a.shape == b.shape
     d = make_layer(tokens=3, hidden=64, experts=4, ffn=600, top_k=2, seed=22).w13(2)
     assert not np.array_equal(a, d)
+
+
+def test_stage_replay_hand_trace():
+    """Two stages whose activation sets swap: the online policy lags one stage (CHR 0), the clairvoyant one hits all."""
+    c = np.zeros((4, 1, 4), int)
+    c[0, 0] = c[1, 0] = [3, 1, 0, 0]
+    c[2, 0] = c[3, 0] = [0, 0, 2, 2]
+    r = oracle.stage_replay(c, np.array([2, 2]), np.array([[-1, -1, 0, 1]]), 2)
+    assert r["slot_history"].tolist() == [[[-1, -1, 0, 1]], [[0, 1, -1, -1]]]
+    assert r["chr_online"] == 0.0 and r["chr_clairvoyant"] == 1.0
+
+
+def test_stage_replay_stable_routing_and_exact_ratio():
+    """Routing fixed on experts {1, 3}: after the first stage the online policy is as good as the clairvoyant one."""
+    c = np.zeros((6, 2, 4), int)
+    c[:, :, 1] = 5
+    c[:, :, 3] = 3
+    r = oracle.stage_replay(c, np.array([1, 2, 3]), np.array([[0, 1, -1, -1], [0, 1, -1, -1]]), 2)
+    # stage 0 (1 step): resident {0,1} -> hits 5 of 8 per call; stages 1-2: resident {1,3} -> 8 of 8
+    assert r["chr_online"] == (2 * 5 + 10 * 8) / (12 * 8)
+    assert r["chr_clairvoyant"] == 1.0
+    assert r["resident"][1:].all(axis=0)[:, [1, 3]].all()
