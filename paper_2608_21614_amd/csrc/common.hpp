@@ -48,6 +48,49 @@ __device__ __forceinline__ f32x4 mfma16x16x32(bf16x8 a, bf16x8 b, f32x4 c) {
     return __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, b, c, 0, 0, 0);
 }
 
+// MFMA operand fragment: 8 consecutive K values of one lane (its row, or its
+// column, and K offset 8*(lane/16) inside a 32-wide K step).  bf16 feeds one
+// 16x16x32 MFMA; fp32 feeds eight 16x16x4 MFMAs, MFMA i taking value i of every
+// lane, i.e. K indices {i, 8+i, 16+i, 24+i} of the step.  Both operands use the
+// same assignment, so every product of the step is summed exactly once.
+template <typename Elt>
+struct Frag8;
+template <>
+struct Frag8<uint16_t> {
+    bf16x8 v;
+};
+template <>
+struct Frag8<float> {
+    f32x4 lo, hi;
+};
+
+__device__ __forceinline__ Frag8<uint16_t> load_frag(const uint16_t* p) { return {load_bf16x8(p)}; }
+__device__ __forceinline__ Frag8<float> load_frag(const float* p) {
+    const f32x4* q = reinterpret_cast<const f32x4*>(p);
+    return {q[0], q[1]};
+}
+template <typename Elt>
+__device__ __forceinline__ Frag8<Elt> zero_frag();
+template <>
+__device__ __forceinline__ Frag8<uint16_t> zero_frag<uint16_t>() { return {zero_bf16x8()}; }
+template <>
+__device__ __forceinline__ Frag8<float> zero_frag<float>() { return {f32x4{0.f, 0.f, 0.f, 0.f}, f32x4{0.f, 0.f, 0.f, 0.f}}; }
+
+__device__ __forceinline__ f32x4 mma_frag(const Frag8<uint16_t>& a, const Frag8<uint16_t>& b, f32x4 c) {
+    return mfma16x16x32(a.v, b.v, c);
+}
+__device__ __forceinline__ f32x4 mma_frag(const Frag8<float>& a, const Frag8<float>& b, f32x4 c) {
+    c = __builtin_amdgcn_mfma_f32_16x16x4f32(a.lo.x, b.lo.x, c, 0, 0, 0);
+    c = __builtin_amdgcn_mfma_f32_16x16x4f32(a.lo.y, b.lo.y, c, 0, 0, 0);
+    c = __builtin_amdgcn_mfma_f32_16x16x4f32(a.lo.z, b.lo.z, c, 0, 0, 0);
+    c = __builtin_amdgcn_mfma_f32_16x16x4f32(a.lo.w, b.lo.w, c, 0, 0, 0);
+    c = __builtin_amdgcn_mfma_f32_16x16x4f32(a.hi.x, b.hi.x, c, 0, 0, 0);
+    c = __builtin_amdgcn_mfma_f32_16x16x4f32(a.hi.y, b.hi.y, c, 0, 0, 0);
+    c = __builtin_amdgcn_mfma_f32_16x16x4f32(a.hi.z, b.hi.z, c, 0, 0, 0);
+    c = __builtin_amdgcn_mfma_f32_16x16x4f32(a.hi.w, b.hi.w, c, 0, 0, 0);
+    return c;
+}
+
 __device__ __forceinline__ float silu(float z) { return z / (1.0f + __expf(-z)); }
 
 __device__ __forceinline__ int lane_id() { return threadIdx.x & (kWave - 1); }

@@ -12,7 +12,7 @@
 // MFMA A operands.
 //
 // Three kernel families:
-//  * stream  (bf16, T <= 64, decode): the weights are streamed from HBM exactly
+//  * stream  (T <= 64, decode; bf16 MFMA 16x16x32, fp32 MFMA 16x16x4): the weights are streamed from HBM exactly
 //    once.  A workgroup owns 32 features (phase 1: 32 gate + 32 up weight
 //    rows) or 64 outputs (phase 2: 64 rows of W2) of one expert; the weights are
 //    the MFMA M side and the expert's tokens the N side, in tiles of 16.  Its
@@ -24,10 +24,11 @@
 //    splits K across workgroups into `ks` chunks whose partial sums the combine
 //    adds in fixed order.  SwiGLU is applied in the phase-1 epilogue, so the gate
 //    and up projections are never stored.
-//  * tiled   (bf16, T > 64, prefill): MFMA tiles of 64 weight rows x 64 tokens,
-//    K staged through LDS in double-buffered 64-wide slabs; the phase-1 tile
-//    holds 16 gate and 16 up rows per wave so SwiGLU runs in registers.
-//  * f32     (fp32 layers): plain fp32 FMA, one output per thread.
+//  * tiled   (bf16, T > 64, prefill): workgroup tiles of 128 weight rows x 128
+//    tokens (64 x 64 per wave), K staged through LDS in double-buffered 64-wide
+//    slabs; each phase-1 wave holds the gate and up rows of the same features so
+//    SwiGLU runs in registers.
+//  * f32     (fp32, T > 64): plain fp32 FMA, one output per thread.
 // All of them read counts and offsets from device memory: the grid is sized for
 // the worst case on the host and surplus workgroups exit at once.
 #include "common.hpp"
@@ -64,17 +65,17 @@ struct Args {
 
 // off_rows[p - n_res] = x[perm[p] / k] and off_w[p - n_res] = topk_w[perm[p]] for the
 // offloaded rows p = n_res + wg, n_res + wg + nwg, ...
-__device__ void pack_offloaded(const Args& a, int wg, int nwg) {
+__device__ void pack_offloaded(const Args& a, int wg, int nwg, int elt) {
     const int P = a.T * a.k;
     const int nres = *a.n_res;
-    const int chunks = a.H / 8;  // 16-byte chunks of a bf16 row
+    const int chunks = a.H * elt / 16;  // 16-byte chunks of a row
     for (int p = nres + wg; p < P; p += nwg) {
         const int q = a.perm[p];
         if (q < 0 || q >= P) continue;
         const int t = q / a.k;
         if (a.off_rows) {
-            const u32x4* src = reinterpret_cast<const u32x4*>(static_cast<const uint16_t*>(a.x) + (size_t)t * a.H);
-            u32x4* dst = reinterpret_cast<u32x4*>(static_cast<uint16_t*>(a.off_rows) + (size_t)(p - nres) * a.H);
+            const u32x4* src = reinterpret_cast<const u32x4*>(static_cast<const uint8_t*>(a.x) + (size_t)t * a.H * elt);
+            u32x4* dst = reinterpret_cast<u32x4*>(static_cast<uint8_t*>(a.off_rows) + (size_t)(p - nres) * a.H * elt);
             for (int c = threadIdx.x; c < chunks; c += blockDim.x) dst[c] = src[c];
         }
         if (a.off_w && threadIdx.x == 0) a.off_w[p - nres] = a.topk_w[q];
@@ -157,10 +158,11 @@ __device__ __forceinline__ int group_token(const Args& a, const Group& g, int n)
 // stream kernel (decode)
 // ---------------------------------------------------------------------------
 
-template <int NT, bool kDown>
+template <typename Elt, int NT, bool kDown>
 __global__ void __launch_bounds__(256) k_ffn_stream(Args a) {
-    constexpr int MT = 4;   // 16-row weight tiles per workgroup
-    constexpr int U = 2;    // K steps per load batch (two batches in flight)
+    using F8 = Frag8<Elt>;
+    constexpr int MT = 4;                          // 16-row weight tiles per workgroup
+    constexpr int U = sizeof(Elt) == 2 ? 2 : 1;    // K steps per load batch (two batches in flight)
     __shared__ int s_list[256];
     __shared__ int s_wsum[4];
     __shared__ f32x4 s_red[4][MT][NT][kWave];
@@ -168,7 +170,7 @@ __global__ void __launch_bounds__(256) k_ffn_stream(Args a) {
     const int item = blockIdx.x;
     const int n_items = a.max_routed * a.ipg_r + a.S * a.ipg_s;
     if (!kDown && item >= n_items) {  // trailing workgroups pack the offloaded rows
-        pack_offloaded(a, item - n_items, gridDim.x - n_items);
+        pack_offloaded(a, item - n_items, gridDim.x - n_items, sizeof(Elt));
         return;
     }
     const int nact = list_active(a, s_list, s_wsum);
@@ -177,13 +179,13 @@ __global__ void __launch_bounds__(256) k_ffn_stream(Args a) {
     if (item < a.max_routed * a.ipg_r) {
         const int gi = item / a.ipg_r;
         if (gi >= nact) return;
-        g = routed_group(a, s_list[gi], 2);
+        g = routed_group(a, s_list[gi], sizeof(Elt));
         sub = item % a.ipg_r;
     } else {
         const int i2 = item - a.max_routed * a.ipg_r;
         const int s = i2 / a.ipg_s;
         if (s >= a.S) return;
-        g = shared_group(a, s, 2);
+        g = shared_group(a, s, sizeof(Elt));
         sub = i2 % a.ipg_s;
     }
     if (g.count == 0) return;
@@ -192,13 +194,13 @@ __global__ void __launch_bounds__(256) k_ffn_stream(Args a) {
     const int r = lane & 15, kq = (lane >> 4) * 8;
 
     // weight tiles of this workgroup (16-row tiles in the tile layout) and the K chunk
-    const uint16_t* wp[MT];
+    const Elt* wp[MT];
     int row0, kc = 0, c0, c1;
     if (!kDown) {
         const int f0 = sub * 32;
         row0 = f0;
         const int nst = a.H / 32;
-        const uint16_t* w = reinterpret_cast<const uint16_t*>(g.w13);
+        const Elt* w = reinterpret_cast<const Elt*>(g.w13);
 #pragma unroll
         for (int m = 0; m < MT; ++m) {
             const int rt = (m < 2 ? 0 : g.Fg / 16) + f0 / 16 + (m & 1);  // gate tiles, then up tiles
@@ -211,7 +213,7 @@ __global__ void __launch_bounds__(256) k_ffn_stream(Args a) {
         kc = sub % a.ks;
         row0 = h0;
         const int nst = g.Fg / 32;
-        const uint16_t* w = reinterpret_cast<const uint16_t*>(g.w2);
+        const Elt* w = reinterpret_cast<const Elt*>(g.w2);
 #pragma unroll
         for (int m = 0; m < MT; ++m) wp[m] = w + (size_t)(h0 / 16 + m) * nst * 512 + lane * 8;
         c0 = kc * nst / a.ks;
@@ -223,16 +225,16 @@ __global__ void __launch_bounds__(256) k_ffn_stream(Args a) {
 
     // token operand rows (N side)
     const int ntile = min(NT, (g.count + 15) / 16);
-    const uint16_t* bp[NT];
+    const Elt* bp[NT];
 #pragma unroll
     for (int j = 0; j < NT; ++j) {
         bp[j] = nullptr;
         const int n = 16 * j + r;
         if (!kDown) {
             const int t = group_token(a, g, n);
-            if (t >= 0) bp[j] = static_cast<const uint16_t*>(a.x) + (size_t)t * a.H + kq;
+            if (t >= 0) bp[j] = static_cast<const Elt*>(a.x) + (size_t)t * a.H + kq;
         } else if (n < g.count) {
-            bp[j] = static_cast<const uint16_t*>(a.act) + (size_t)(g.rowbase + n) * a.Fa + kq;
+            bp[j] = static_cast<const Elt*>(a.act) + (size_t)(g.rowbase + n) * a.Fa + kq;
         }
     }
 
@@ -243,28 +245,28 @@ __global__ void __launch_bounds__(256) k_ffn_stream(Args a) {
         for (int j = 0; j < NT; ++j) acc[m][j] = f32x4{0.f, 0.f, 0.f, 0.f};
 
     // batch b holds this wave's steps i = U*b .. U*b+U-1
-    auto load = [&](bf16x8 (&A)[U][MT], bf16x8 (&B)[U][NT], int b) {
+    auto load = [&](F8 (&A)[U][MT], F8 (&B)[U][NT], int b) {
 #pragma unroll
         for (int u = 0; u < U; ++u) {
             const int s = sbase + 4 * (U * b + u);
 #pragma unroll
-            for (int m = 0; m < MT; ++m) A[u][m] = load_bf16x8(wp[m] + (size_t)s * 512);
+            for (int m = 0; m < MT; ++m) A[u][m] = load_frag(wp[m] + (size_t)s * 512);
 #pragma unroll
-            for (int j = 0; j < NT; ++j) B[u][j] = (j < ntile && bp[j]) ? load_bf16x8(bp[j] + s * 32) : zero_bf16x8();
+            for (int j = 0; j < NT; ++j) B[u][j] = (j < ntile && bp[j]) ? load_frag(bp[j] + s * 32) : zero_frag<Elt>();
         }
     };
-    auto mma = [&](const bf16x8 (&A)[U][MT], const bf16x8 (&B)[U][NT]) {
+    auto mma = [&](const F8 (&A)[U][MT], const F8 (&B)[U][NT]) {
         // tiles past the group's last token see zero operands: no branch, fewer live registers
 #pragma unroll
         for (int u = 0; u < U; ++u)
 #pragma unroll
             for (int j = 0; j < NT; ++j)
 #pragma unroll
-                for (int m = 0; m < MT; ++m) acc[m][j] = mfma16x16x32(A[u][m], B[u][j], acc[m][j]);
+                for (int m = 0; m < MT; ++m) acc[m][j] = mma_frag(A[u][m], B[u][j], acc[m][j]);
     };
     const int nb = n_my / U;
     {
-        bf16x8 A0[U][MT], B0[U][NT], A1[U][MT], B1[U][NT];
+        F8 A0[U][MT], B0[U][NT], A1[U][MT], B1[U][NT];
         if (nb > 0) load(A0, B0, 0);
         for (int b = 0; b < nb; b += 2) {
             if (b + 1 < nb) load(A1, B1, b + 1);
@@ -275,15 +277,15 @@ __global__ void __launch_bounds__(256) k_ffn_stream(Args a) {
     }
     for (int i = nb * U; i < n_my; ++i) {
         const int s = sbase + 4 * i;
-        bf16x8 A[MT], B[NT];
+        F8 A[MT], B[NT];
 #pragma unroll
-        for (int m = 0; m < MT; ++m) A[m] = load_bf16x8(wp[m] + (size_t)s * 512);
+        for (int m = 0; m < MT; ++m) A[m] = load_frag(wp[m] + (size_t)s * 512);
 #pragma unroll
-        for (int j = 0; j < NT; ++j) B[j] = (j < ntile && bp[j]) ? load_bf16x8(bp[j] + s * 32) : zero_bf16x8();
+        for (int j = 0; j < NT; ++j) B[j] = (j < ntile && bp[j]) ? load_frag(bp[j] + s * 32) : zero_frag<Elt>();
 #pragma unroll
         for (int j = 0; j < NT; ++j)
 #pragma unroll
-            for (int m = 0; m < MT; ++m) acc[m][j] = mfma16x16x32(A[m], B[j], acc[m][j]);
+            for (int m = 0; m < MT; ++m) acc[m][j] = mma_frag(A[m], B[j], acc[m][j]);
     }
 
 #pragma unroll
@@ -307,11 +309,16 @@ __global__ void __launch_bounds__(256) k_ffn_stream(Args a) {
                 uv += s_red[w][m + 2][j][l];
             }
             const int f = row0 + 16 * m + 4 * (l >> 4);
-            u32x2 packed;
-            packed.x = pack_bf16x2(silu(gv.x) * uv.x, silu(gv.y) * uv.y);
-            packed.y = pack_bf16x2(silu(gv.z) * uv.z, silu(gv.w) * uv.w);
-            uint16_t* dst = static_cast<uint16_t*>(a.act) + (size_t)(g.rowbase + n) * a.Fa + f;
-            *reinterpret_cast<u32x2*>(dst) = packed;
+            const f32x4 av = {silu(gv.x) * uv.x, silu(gv.y) * uv.y, silu(gv.z) * uv.z, silu(gv.w) * uv.w};
+            Elt* dst = static_cast<Elt*>(a.act) + (size_t)(g.rowbase + n) * a.Fa + f;
+            if constexpr (sizeof(Elt) == 2) {
+                u32x2 packed;
+                packed.x = pack_bf16x2(av.x, av.y);
+                packed.y = pack_bf16x2(av.z, av.w);
+                *reinterpret_cast<u32x2*>(dst) = packed;
+            } else {
+                *reinterpret_cast<f32x4*>(dst) = av;
+            }
         }
     } else {
         for (int task = threadIdx.x; task < MT * NT * kWave; task += 256) {
@@ -334,13 +341,13 @@ __global__ void __launch_bounds__(256) k_ffn_stream(Args a) {
 // tiled kernel (prefill)
 // ---------------------------------------------------------------------------
 
-constexpr int kTn = 64;      // tokens per tile
-constexpr int kTk = 64;      // K slab
-constexpr int kPitch = kTk + 8;  // LDS row pitch (bf16 elements)
+constexpr int kTn = 128;         // tokens per tile
+constexpr int kTk = 64;          // K slab
+constexpr int kXPitch = kTk + 8;  // LDS row pitch of the token tile (bf16 elements)
 
-// Active routed experts and the prefix of their 64-token tile counts.
+// Active routed experts and the prefix of their kTn-token tile counts.
 __device__ int list_tiles(const Args& a, int* s_list, int* s_wsum, int* s_tpre, int nact) {
-    // s_tpre[g] = sum_{g' < g} ceil(count(g') / 64); s_tpre[nact] = total
+    // s_tpre[g] = sum_{g' < g} ceil(count(g') / kTn); s_tpre[nact] = total
     if (threadIdx.x < 64) {
         const int lane = threadIdx.x;
         int v[4], sum = 0;
@@ -375,17 +382,28 @@ __device__ int list_tiles(const Args& a, int* s_list, int* s_wsum, int* s_tpre, 
     return s_wsum[0];
 }
 
+// Workgroup tile: 128 weight rows x 128 tokens; phase 1 takes 64 features (their
+// 64 gate rows and 64 up rows), phase 2 128 rows of W2.  Four waves in 2 x 2,
+// each 64 rows x 64 tokens (16 MFMA 16x16x32 tiles, 64 fp32 accumulators per
+// lane); phase-1 waves hold the gate and up rows of the same 32 features so
+// SwiGLU runs in registers.  K runs in 64-wide slabs, double-buffered in LDS:
+// the weight slab is 16 blocks of 1 KB copied as they sit in the tile layout,
+// the token slab 128 gathered rows.  Consecutive tiles (same token tile, next
+// weight tile) are placed on the same XCD so they share its L2.
 template <bool kDown>
-__global__ void __launch_bounds__(256) k_ffn_tiled(Args a, int max_rtiles, int ntn_r, int ntn_s) {
+__global__ void __launch_bounds__(256) k_ffn_tiled(Args a, int max_rtiles, int ntn_r, int ntn_s, int grid8) {
     __shared__ int s_list[256];
     __shared__ int s_wsum[4];
     __shared__ int s_tpre[260];
-    __shared__ __attribute__((aligned(16))) uint16_t sW[2][8][512];
-    __shared__ __attribute__((aligned(16))) uint16_t sX[2][kTn][kPitch];
+    __shared__ __attribute__((aligned(16))) uint16_t sW[2][16][512];
+    __shared__ __attribute__((aligned(16))) uint16_t sX[2][kTn][kXPitch];
 
     const int nact = list_active(a, s_list, s_wsum);
     const int total_rt = list_tiles(a, s_list, s_wsum, s_tpre, nact);
-    const int item = blockIdx.x;
+    // XCD-aware order: workgroups are dealt to the 8 XCDs round-robin, so logical
+    // items pid/8, pid/8 + 1, ... of one XCD are consecutive in this numbering.
+    const int pid = blockIdx.x;
+    const int item = (pid % 8) * (grid8 / 8) + pid / 8;
     Group g;
     int mt_local, wn;
     if (item < max_rtiles * ntn_r) {
@@ -415,34 +433,28 @@ __global__ void __launch_bounds__(256) k_ffn_tiled(Args a, int max_rtiles, int n
 
     const int tid = threadIdx.x, wave = tid >> 6, lane = lane_id();
     const int K = kDown ? g.Fg : a.H;
-    const uint16_t* wbase = reinterpret_cast<const uint16_t*>(kDown ? g.w2 : g.w13);
-    const int wrow0 = wn * (kDown ? 64 : 32);  // first output feature (phase 1) or output row (phase 2)
-
-    // global -> LDS copy assignment, 2 chunks of 16 B per thread per tile:
-    // W: 8 blocks of 1 KB (4 row tiles x 2 K steps of the 64-wide slab), copied as is;
-    // X: 64 token rows x 64 columns.
     const int nst = K / 32;
-    int rt_of[4];
-    if (!kDown) {
-        const int t0 = wrow0 / 16;  // wrow0 = first feature of the tile
-        rt_of[0] = t0;
-        rt_of[1] = t0 + 1;
-        rt_of[2] = g.Fg / 16 + t0;
-        rt_of[3] = g.Fg / 16 + t0 + 1;
-    } else {
+    const uint16_t* wbase = reinterpret_cast<const uint16_t*>(kDown ? g.w2 : g.w13);
+    const int wrow0 = wn * (kDown ? 128 : 64);  // first output row (phase 2) or feature (phase 1)
+    const int rows_total = kDown ? a.H : 2 * g.Fg;
+
+    // the 8 row tiles of the weight slab: phase 1 gate f0/16 + 0..3, then up; phase 2 h0/16 + 0..7
+    int rt_of[8];
 #pragma unroll
-        for (int i = 0; i < 4; ++i) rt_of[i] = wrow0 / 16 + i;
-    }
-    const uint16_t* gW[2];
-    const uint16_t* gX[2];
-    int wb[2], wl[2], cr[2], cc[2];
+    for (int i = 0; i < 8; ++i)
+        rt_of[i] = kDown ? wrow0 / 16 + i : (i < 4 ? 0 : g.Fg / 16) + wrow0 / 16 + (i & 3);
+
+    // global -> LDS copy assignment, 4 chunks of 16 B per thread per operand
+    const uint16_t* gW[4];
+    const uint16_t* gX[4];
+    int wb[4], wl[4], cr[4], cc[4];
 #pragma unroll
-    for (int i = 0; i < 2; ++i) {
+    for (int i = 0; i < 4; ++i) {
         const int c = tid + 256 * i;
         wb[i] = c >> 6;
         wl[i] = c & 63;
         const int rtl = wb[i] >> 1, ks = wb[i] & 1;
-        gW[i] = wbase + ((size_t)rt_of[rtl] * nst + ks) * 512 + wl[i] * 8;
+        gW[i] = (16 * rt_of[rtl] < rows_total) ? wbase + ((size_t)rt_of[rtl] * nst + ks) * 512 + wl[i] * 8 : nullptr;
         cr[i] = c >> 3;
         cc[i] = (c & 7) * 8;
         const int n = n0 + cr[i];
@@ -457,24 +469,27 @@ __global__ void __launch_bounds__(256) k_ffn_tiled(Args a, int max_rtiles, int n
 
     const int wr = wave >> 1, wc = wave & 1;
     const int r = lane & 15, kq = (lane >> 4) * 8;
-    f32x4 acc[2][2];
+    int rtl_of[4];
 #pragma unroll
-    for (int m = 0; m < 2; ++m)
+    for (int m = 0; m < 4; ++m) rtl_of[m] = kDown ? 4 * wr + m : (m < 2 ? 2 * wr + m : 4 + 2 * wr + (m - 2));
+    f32x4 acc[4][4];
 #pragma unroll
-        for (int j = 0; j < 2; ++j) acc[m][j] = f32x4{0.f, 0.f, 0.f, 0.f};
+    for (int m = 0; m < 4; ++m)
+#pragma unroll
+        for (int j = 0; j < 4; ++j) acc[m][j] = f32x4{0.f, 0.f, 0.f, 0.f};
 
     const int nk = K / kTk;
-    u32x4 rw[2], rx[2];
+    u32x4 rw[4], rx[4];
     auto gload = [&](int kt) {
 #pragma unroll
-        for (int i = 0; i < 2; ++i) {
-            rw[i] = *reinterpret_cast<const u32x4*>(gW[i] + (size_t)kt * 2 * 512);
+        for (int i = 0; i < 4; ++i) {
+            rw[i] = gW[i] ? *reinterpret_cast<const u32x4*>(gW[i] + (size_t)kt * 2 * 512) : u32x4{0u, 0u, 0u, 0u};
             rx[i] = gX[i] ? *reinterpret_cast<const u32x4*>(gX[i] + kt * kTk) : u32x4{0u, 0u, 0u, 0u};
         }
     };
     auto lstore = [&](int buf) {
 #pragma unroll
-        for (int i = 0; i < 2; ++i) {
+        for (int i = 0; i < 4; ++i) {
             *reinterpret_cast<u32x4*>(&sW[buf][wb[i]][wl[i] * 8]) = rw[i];
             *reinterpret_cast<u32x4*>(&sX[buf][cr[i]][cc[i]]) = rx[i];
         }
@@ -488,42 +503,42 @@ __global__ void __launch_bounds__(256) k_ffn_tiled(Args a, int max_rtiles, int n
         if (kt + 1 < nk) gload(kt + 1);
 #pragma unroll
         for (int ks = 0; ks < kTk / 32; ++ks) {
-            bf16x8 A[2], B[2];
+            bf16x8 A[4], B[4];
 #pragma unroll
-            for (int m = 0; m < 2; ++m) {
-                // phase 1: gate tile wr and up tile wr (same features); phase 2: tiles 2wr, 2wr+1
-                const int rtl = kDown ? 2 * wr + m : (m == 0 ? wr : 2 + wr);
-                A[m] = __builtin_bit_cast(bf16x8, *reinterpret_cast<const u32x4*>(&sW[buf][rtl * 2 + ks][lane * 8]));
-            }
+            for (int m = 0; m < 4; ++m)
+                A[m] = __builtin_bit_cast(bf16x8, *reinterpret_cast<const u32x4*>(&sW[buf][rtl_of[m] * 2 + ks][lane * 8]));
 #pragma unroll
-            for (int j = 0; j < 2; ++j)
-                B[j] = __builtin_bit_cast(bf16x8, *reinterpret_cast<const u32x4*>(&sX[buf][32 * wc + 16 * j + r][ks * 32 + kq]));
+            for (int j = 0; j < 4; ++j)
+                B[j] = __builtin_bit_cast(bf16x8, *reinterpret_cast<const u32x4*>(&sX[buf][64 * wc + 16 * j + r][ks * 32 + kq]));
 #pragma unroll
-            for (int m = 0; m < 2; ++m)
+            for (int m = 0; m < 4; ++m)
 #pragma unroll
-                for (int j = 0; j < 2; ++j) acc[m][j] = mfma16x16x32(A[m], B[j], acc[m][j]);
+                for (int j = 0; j < 4; ++j) acc[m][j] = mfma16x16x32(A[m], B[j], acc[m][j]);
         }
         if (kt + 1 < nk) lstore(buf ^ 1);
         __syncthreads();
     }
 
 #pragma unroll
-    for (int j = 0; j < 2; ++j) {
-        const int n = n0 + 32 * wc + 16 * j + r;
+    for (int j = 0; j < 4; ++j) {
+        const int n = n0 + 64 * wc + 16 * j + r;
         if (n >= g.count) continue;
         if (!kDown) {
-            // acc[0] = gate, acc[1] = up for features wrow0 + 16*wr + 4*(lane/16) + i
-            const f32x4 gv = acc[0][j], uv = acc[1][j];
-            const int f = wrow0 + 16 * wr + 4 * (lane >> 4);
-            u32x2 packed;
-            packed.x = pack_bf16x2(silu(gv.x) * uv.x, silu(gv.y) * uv.y);
-            packed.y = pack_bf16x2(silu(gv.z) * uv.z, silu(gv.w) * uv.w);
-            *reinterpret_cast<u32x2*>(static_cast<uint16_t*>(a.act) + (size_t)(g.rowbase + n) * a.Fa + f) = packed;
-        } else {
+            // acc[m] = gate, acc[m + 2] = up, features wrow0 + 16 (2 wr + m) + 4 (lane/16) + i
 #pragma unroll
             for (int m = 0; m < 2; ++m) {
-                const int h = wrow0 + 32 * wr + 16 * m + 4 * (lane >> 4);
-                *reinterpret_cast<f32x4*>(a.y + (size_t)(g.rowbase + n) * a.H + h) = acc[m][j];
+                const f32x4 gv = acc[m][j], uv = acc[m + 2][j];
+                const int f = wrow0 + 16 * (2 * wr + m) + 4 * (lane >> 4);
+                u32x2 packed;
+                packed.x = pack_bf16x2(silu(gv.x) * uv.x, silu(gv.y) * uv.y);
+                packed.y = pack_bf16x2(silu(gv.z) * uv.z, silu(gv.w) * uv.w);
+                *reinterpret_cast<u32x2*>(static_cast<uint16_t*>(a.act) + (size_t)(g.rowbase + n) * a.Fa + f) = packed;
+            }
+        } else {
+#pragma unroll
+            for (int m = 0; m < 4; ++m) {
+                const int h = wrow0 + 16 * (4 * wr + m) + 4 * (lane >> 4);
+                if (h < a.H) *reinterpret_cast<f32x4*>(a.y + (size_t)(g.rowbase + n) * a.H + h) = acc[m][j];
             }
         }
     }
@@ -628,7 +643,17 @@ int max_routed_groups(const Shape& s) {
     return m < pairs ? m : pairs;
 }
 
-bool use_stream(const Shape& s) { return s.bf16 && s.T <= 64; }
+bool use_stream(const Shape& s) { return s.T <= 64; }
+
+template <typename Elt, bool kDown>
+void launch_stream(int nt, int grid, const Args& a, hipStream_t st) {
+    switch (nt) {
+        case 1: hipLaunchKernelGGL((k_ffn_stream<Elt, 1, kDown>), dim3(grid), dim3(256), 0, st, a); break;
+        case 2: hipLaunchKernelGGL((k_ffn_stream<Elt, 2, kDown>), dim3(grid), dim3(256), 0, st, a); break;
+        case 3: hipLaunchKernelGGL((k_ffn_stream<Elt, 3, kDown>), dim3(grid), dim3(256), 0, st, a); break;
+        default: hipLaunchKernelGGL((k_ffn_stream<Elt, 4, kDown>), dim3(grid), dim3(256), 0, st, a); break;
+    }
+}
 
 }  // namespace
 
@@ -664,7 +689,7 @@ hipError_t launch_grouped_ffn(const Shape& s, const FfnArgs& fa, hipStream_t st,
     a.n_res = fa.n_res;
     a.off_rows = fa.off_rows;
     a.off_w = fa.off_w;
-    if (!s.bf16) {
+    if (!s.bf16 && !use_stream(s)) {  // fp32 prefill: plain FMA kernels
         a.ipg_r = a.ipg_s = 1;
         const int groups = a.max_routed + s.S;
         if (groups == 0) return hipSuccess;
@@ -685,12 +710,8 @@ hipError_t launch_grouped_ffn(const Shape& s, const FfnArgs& fa, hipStream_t st,
             grid += P < 64 ? P : 64;  // pack workgroups (P >= 1 here)
         }
         if (grid > 0) {
-            switch (nt) {
-                case 1: hipLaunchKernelGGL((k_ffn_stream<1, false>), dim3(grid), dim3(256), 0, st, a); break;
-                case 2: hipLaunchKernelGGL((k_ffn_stream<2, false>), dim3(grid), dim3(256), 0, st, a); break;
-                case 3: hipLaunchKernelGGL((k_ffn_stream<3, false>), dim3(grid), dim3(256), 0, st, a); break;
-                default: hipLaunchKernelGGL((k_ffn_stream<4, false>), dim3(grid), dim3(256), 0, st, a); break;
-            }
+            if (s.bf16) launch_stream<uint16_t, false>(nt, grid, a, st);
+            else launch_stream<float, false>(nt, grid, a, st);
         }
         if (hipError_t e = mark(); e != hipSuccess) return e;
         // phase 2: 64 output rows x one K chunk per workgroup
@@ -698,30 +719,31 @@ hipError_t launch_grouped_ffn(const Shape& s, const FfnArgs& fa, hipStream_t st,
         a.ipg_s = (s.H / 64) * a.ks;
         grid = a.max_routed * a.ipg_r + s.S * a.ipg_s;
         if (grid > 0) {
-            switch (nt) {
-                case 1: hipLaunchKernelGGL((k_ffn_stream<1, true>), dim3(grid), dim3(256), 0, st, a); break;
-                case 2: hipLaunchKernelGGL((k_ffn_stream<2, true>), dim3(grid), dim3(256), 0, st, a); break;
-                case 3: hipLaunchKernelGGL((k_ffn_stream<3, true>), dim3(grid), dim3(256), 0, st, a); break;
-                default: hipLaunchKernelGGL((k_ffn_stream<4, true>), dim3(grid), dim3(256), 0, st, a); break;
-            }
+            if (s.bf16) launch_stream<uint16_t, true>(nt, grid, a, st);
+            else launch_stream<float, true>(nt, grid, a, st);
         }
         return hipGetLastError();
     }
-    // tiled: worst-case number of 64-token tiles over the routed groups
+    // tiled: worst-case number of kTn-token tiles over the routed groups
     const int P = s.T * s.k;
     const int max_rtiles = (a.max_routed == 0) ? 0 : (P + kTn - 1) / kTn + a.max_routed;
     const int tps = (s.T + kTn - 1) / kTn;
     a.ipg_r = a.ipg_s = 0;
+    auto round8 = [](long long n) { return (n + 7) / 8 * 8; };
     {
-        const int ntn_r = s.F / 32, ntn_s = s.S > 0 ? s.Fs / 32 : 0;
-        const long long grid = (long long)max_rtiles * ntn_r + (long long)s.S * tps * ntn_s;
-        if (grid > 0) hipLaunchKernelGGL((k_ffn_tiled<false>), dim3((unsigned)grid), dim3(256), 0, st, a, max_rtiles, ntn_r, ntn_s > 0 ? ntn_s : 1);
+        const int ntn_r = s.F / 64, ntn_s = s.S > 0 ? s.Fs / 64 : 1;
+        const long long grid = round8((long long)max_rtiles * ntn_r + (long long)s.S * tps * ntn_s);
+        if (grid > 0)
+            hipLaunchKernelGGL((k_ffn_tiled<false>), dim3((unsigned)grid), dim3(256), 0, st, a, max_rtiles, ntn_r,
+                               ntn_s, (int)grid);
     }
     if (hipError_t e = mark(); e != hipSuccess) return e;
     {
-        const int ntn = s.H / 64;
-        const long long grid = (long long)max_rtiles * ntn + (long long)s.S * tps * ntn;
-        if (grid > 0) hipLaunchKernelGGL((k_ffn_tiled<true>), dim3((unsigned)grid), dim3(256), 0, st, a, max_rtiles, ntn, ntn);
+        const int ntn = (s.H + 127) / 128;
+        const long long grid = round8((long long)max_rtiles * ntn + (long long)s.S * tps * ntn);
+        if (grid > 0)
+            hipLaunchKernelGGL((k_ffn_tiled<true>), dim3((unsigned)grid), dim3(256), 0, st, a, max_rtiles, ntn, ntn,
+                               (int)grid);
     }
     return hipGetLastError();
 }
