@@ -174,19 +174,19 @@ __global__ void __launch_bounds__(256) k_ffn_stream(Args a) {
         return;
     }
     const int nact = list_active(a, s_list, s_wsum);
+    // shared groups first: their items can be longer (Fs > F in phase 2), so they
+    // start in the first wave of workgroups instead of forming a tail
     Group g;
     int sub;
-    if (item < a.max_routed * a.ipg_r) {
-        const int gi = item / a.ipg_r;
+    if (item < a.S * a.ipg_s) {
+        g = shared_group(a, item / a.ipg_s, sizeof(Elt));
+        sub = item % a.ipg_s;
+    } else {
+        const int i2 = item - a.S * a.ipg_s;
+        const int gi = i2 / a.ipg_r;
         if (gi >= nact) return;
         g = routed_group(a, s_list[gi], sizeof(Elt));
-        sub = item % a.ipg_r;
-    } else {
-        const int i2 = item - a.max_routed * a.ipg_r;
-        const int s = i2 / a.ipg_s;
-        if (s >= a.S) return;
-        g = shared_group(a, s, sizeof(Elt));
-        sub = i2 % a.ipg_s;
+        sub = i2 % a.ipg_r;
     }
     if (g.count == 0) return;
 

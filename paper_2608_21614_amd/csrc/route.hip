@@ -49,54 +49,44 @@ __global__ void __launch_bounds__(kFrontThreads)
 }
 
 // Decode batches: part[slice][t][e] = sum over the slice's K steps of x[t] . w_router[e].
-// One workgroup per K slice; wave w covers tokens 16w .. 16w+15.
-template <bool kBf16>
+// One workgroup per K slice; wave w covers tokens 16w .. 16w+15; MFMA on bf16
+// (16x16x32) or fp32 (16x16x4) operands.
+template <typename Elt>
 __global__ void __launch_bounds__(256)
     k_router_partial(int T, int H, int E, const void* __restrict__ x, const void* __restrict__ wr, int nsl,
                      float* __restrict__ part) {
     const int slice = blockIdx.x;
     const int nst = H / 32, s0 = slice * nst / nsl, s1 = (slice + 1) * nst / nsl;
     float* out = part + (size_t)slice * 64 * E;
-    if (!kBf16) {
-        const float* xf = static_cast<const float*>(x);
-        const float* wf = static_cast<const float*>(wr);
-        for (int idx = threadIdx.x; idx < T * E; idx += blockDim.x) {
-            const int t = idx / E, e = idx % E;
-            float acc = 0.f;
-            for (int h = 32 * s0; h < 32 * s1; ++h) acc = fmaf(xf[(size_t)t * H + h], wf[(size_t)e * H + h], acc);
-            out[t * E + e] = acc;
-        }
-        return;
-    }
     const int wave = threadIdx.x >> 6, lane = lane_id();
     const int r = lane & 15, kq = (lane >> 4) * 8;
     if (16 * wave >= T) return;
     const int tok = 16 * wave + r;
-    const uint16_t* xp = (tok < T) ? static_cast<const uint16_t*>(x) + (size_t)tok * H + kq : nullptr;
+    const Elt* xp = (tok < T) ? static_cast<const Elt*>(x) + (size_t)tok * H + kq : nullptr;
     for (int c0 = 0; c0 < E; c0 += kScoreChunk) {
         f32x4 acc[4];
-        const uint16_t* wp[4];
+        const Elt* wp[4];
 #pragma unroll
         for (int m = 0; m < 4; ++m) {
             acc[m] = f32x4{0.f, 0.f, 0.f, 0.f};
             const int e = c0 + 16 * m + r;
-            wp[m] = (e < E) ? static_cast<const uint16_t*>(wr) + (size_t)e * H + kq : nullptr;
+            wp[m] = (e < E) ? static_cast<const Elt*>(wr) + (size_t)e * H + kq : nullptr;
         }
         for (int s = s0; s < s1; s += 4) {
-            bf16x8 A[4][4], B[4];
+            Frag8<Elt> A[4][4], B[4];
 #pragma unroll
             for (int u = 0; u < 4; ++u) {
                 const bool ok = s + u < s1;
-                B[u] = (ok && xp) ? load_bf16x8(xp + (s + u) * 32) : zero_bf16x8();
+                B[u] = (ok && xp) ? load_frag(xp + (s + u) * 32) : zero_frag<Elt>();
 #pragma unroll
                 for (int m = 0; m < 4; ++m)
-                    A[u][m] = (ok && wp[m]) ? load_bf16x8(wp[m] + (s + u) * 32) : zero_bf16x8();
+                    A[u][m] = (ok && wp[m]) ? load_frag(wp[m] + (s + u) * 32) : zero_frag<Elt>();
             }
 #pragma unroll
             for (int u = 0; u < 4; ++u)
 #pragma unroll
                 for (int m = 0; m < 4; ++m)
-                    if (c0 + 16 * m < E) acc[m] = mfma16x16x32(A[u][m], B[u], acc[m]);
+                    if (c0 + 16 * m < E) acc[m] = mma_frag(A[u][m], B[u], acc[m]);
         }
         if (tok < T) {
 #pragma unroll
@@ -173,10 +163,10 @@ hipError_t launch_small(const Shape& s, const void* x, const void* w_router, con
     const int nsl = router_slices(s);
     if (!logits_in && s.T > 0) {
         if (s.bf16)
-            hipLaunchKernelGGL(k_router_partial<true>, dim3(nsl), dim3(256), 0, st, s.T, s.H, s.E, x, w_router, nsl,
-                               part);
+            hipLaunchKernelGGL(k_router_partial<uint16_t>, dim3(nsl), dim3(256), 0, st, s.T, s.H, s.E, x, w_router,
+                               nsl, part);
         else
-            hipLaunchKernelGGL(k_router_partial<false>, dim3(nsl), dim3(256), 0, st, s.T, s.H, s.E, x, w_router, nsl,
+            hipLaunchKernelGGL(k_router_partial<float>, dim3(nsl), dim3(256), 0, st, s.T, s.H, s.E, x, w_router, nsl,
                                part);
     }
     hipLaunchKernelGGL(k_front_small, dim3(1), dim3(kFrontThreads), 0, st, s.T, s.E, s.k, s.slots, part, nsl, bias,
