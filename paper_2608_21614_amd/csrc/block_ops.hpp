@@ -14,14 +14,30 @@ constexpr int kFrontWaves = kFrontThreads / kWave;
 constexpr int kLgPitch = 257;                   // LDS row pitch of a score tile (E <= 256)
 constexpr int kScoreChunk = 64;                 // experts (4 MFMA row tiles) per reduction pass
 
+// Maximum over the wave: DPP within each row of 16 lanes, then the four row
+// maxima (every lane gets the result).  NaN inputs are ignored by fmaxf.
+__device__ __forceinline__ float wave_max(float v) {
+    v = fmaxf(v, __int_as_float(__builtin_amdgcn_mov_dpp(__float_as_int(v), 0xB1, 0xF, 0xF, false)));   // quad_perm 1,0,3,2
+    v = fmaxf(v, __int_as_float(__builtin_amdgcn_mov_dpp(__float_as_int(v), 0x4E, 0xF, 0xF, false)));   // quad_perm 2,3,0,1
+    v = fmaxf(v, __int_as_float(__builtin_amdgcn_mov_dpp(__float_as_int(v), 0x124, 0xF, 0xF, false)));  // row_ror 4
+    v = fmaxf(v, __int_as_float(__builtin_amdgcn_mov_dpp(__float_as_int(v), 0x128, 0xF, 0xF, false)));  // row_ror 8
+    const float r0 = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v), 0));
+    const float r1 = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v), 16));
+    const float r2 = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v), 32));
+    const float r3 = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v), 48));
+    return fmaxf(fmaxf(r0, r1), fmaxf(r2, r3));
+}
+
 // LDS the top-k needs: selected (score, expert) of up to 64 rows x 8.
 constexpr int kTopkLdsWords = 2 * 64 * 8;
 
 // Top-k gate of `rows` tokens whose scores sit in LDS (s_lg, pitch kLgPitch),
 // by the whole workgroup.  Experts are totally ordered by (score desc, expert
 // id asc); the rank of expert e in row t is the number of experts before it in
-// that order, computed for every (t, e) in parallel, and e is the j-th choice
-// of t iff its rank is j < k.  The gate of choice j is exp(s_j - s_0) /
+// that order, and e is the j-th choice of t iff its rank is j < k.  For E <= 64
+// one wave per token with one expert per lane picks the choices in rank order
+// (k rounds of a wave argmax); for larger E every (t, e) counts its rank in
+// parallel.  The gate of choice j is exp(s_j - s_0) /
 // sum_j' exp(s_j' - s_0), summed in j order; a score equal to the top one
 // contributes exactly 1 (so all-equal rows, -inf included, get 1/k).
 // Writes out_idx/out_w rows [t0, t0 + rows) and, if given, lds_idx[t*k + j].
@@ -31,18 +47,39 @@ __device__ inline void topk_rank_block(const float* s_lg, int rows, int E, int k
                                        float* out_w, int32_t* lds_idx, float* s_selv, int* s_sele) {
     for (int i = threadIdx.x; i < rows * 8; i += blockDim.x) s_sele[i] = -1;
     __syncthreads();
-    for (int idx = threadIdx.x; idx < rows * E; idx += blockDim.x) {
-        const int t = idx / E, e = idx % E;
-        const float* row = s_lg + t * kLgPitch;
-        const float v = row[e];
-        int rank = 0;
-        for (int e2 = 0; e2 < E; ++e2) {
-            const float v2 = row[e2];
-            rank += (v2 > v || (v2 == v && e2 < e)) ? 1 : 0;
+    if (E <= kWave) {
+        // one wave per row, lane e holds score e; round j takes the largest
+        // score among the experts not yet chosen (wave max) and, among equal
+        // scores, the lowest expert id (lowest set bit of a ballot)
+        const int lane = lane_id(), nw = blockDim.x / kWave;
+        for (int t = threadIdx.x / kWave; t < rows; t += nw) {
+            const float v = (lane < E) ? s_lg[t * kLgPitch + lane] : 0.f;
+            bool open = lane < E;
+            for (int j = 0; j < k; ++j) {
+                const float m = wave_max(open ? v : -INFINITY);
+                const unsigned long long cand = __ballot(open && v == m);
+                const int e = cand ? __ffsll((long long)cand) - 1 : -1;
+                if (lane == e) open = false;
+                if (lane == 0 && e >= 0) {
+                    s_selv[t * 8 + j] = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v), e));
+                    s_sele[t * 8 + j] = e;
+                }
+            }
         }
-        if (rank < k) {
-            s_selv[t * 8 + rank] = v;
-            s_sele[t * 8 + rank] = e;
+    } else {
+        for (int idx = threadIdx.x; idx < rows * E; idx += blockDim.x) {
+            const int t = idx / E, e = idx % E;
+            const float* row = s_lg + t * kLgPitch;
+            const float v = row[e];
+            int rank = 0;
+            for (int e2 = 0; e2 < E; ++e2) {
+                const float v2 = row[e2];
+                rank += (v2 > v || (v2 == v && e2 < e)) ? 1 : 0;
+            }
+            if (rank < k) {
+                s_selv[t * 8 + rank] = v;
+                s_sele[t * 8 + rank] = e;
+            }
         }
     }
     __syncthreads();

@@ -386,17 +386,17 @@ __device__ int list_tiles(const Args& a, int* s_list, int* s_wsum, int* s_tpre, 
 // 64 gate rows and 64 up rows), phase 2 128 rows of W2.  Four waves in 2 x 2,
 // each 64 rows x 64 tokens (16 MFMA 16x16x32 tiles, 64 fp32 accumulators per
 // lane); phase-1 waves hold the gate and up rows of the same 32 features so
-// SwiGLU runs in registers.  K runs in 64-wide slabs, double-buffered in LDS:
+// SwiGLU runs in registers.  K runs in 64-wide slabs through one LDS buffer:
 // the weight slab is 16 blocks of 1 KB copied as they sit in the tile layout,
-// the token slab 128 gathered rows.  Consecutive tiles (same token tile, next
-// weight tile) are placed on the same XCD so they share its L2.
+// the token slab 128 gathered rows.  Consecutive tiles (same weight tile, next
+// token tile of the group) are placed on the same XCD so they share its L2.
 template <bool kDown>
-__global__ void __launch_bounds__(256) k_ffn_tiled(Args a, int max_rtiles, int ntn_r, int ntn_s, int grid8) {
+__global__ void __launch_bounds__(256, 3) k_ffn_tiled(Args a, int max_rtiles, int ntn_r, int ntn_s, int grid8) {
     __shared__ int s_list[256];
     __shared__ int s_wsum[4];
     __shared__ int s_tpre[260];
-    __shared__ __attribute__((aligned(16))) uint16_t sW[2][16][512];
-    __shared__ __attribute__((aligned(16))) uint16_t sX[2][kTn][kXPitch];
+    __shared__ __attribute__((aligned(16))) uint16_t sW[16][512];
+    __shared__ __attribute__((aligned(16))) uint16_t sX[kTn][kXPitch];
 
     const int nact = list_active(a, s_list, s_wsum);
     const int total_rt = list_tiles(a, s_list, s_wsum, s_tpre, nact);
@@ -406,27 +406,32 @@ __global__ void __launch_bounds__(256) k_ffn_tiled(Args a, int max_rtiles, int n
     const int item = (pid % 8) * (grid8 / 8) + pid / 8;
     Group g;
     int mt_local, wn;
+    // inside a group, items run weight tile by weight tile and, for each, over
+    // all of the group's token tiles: the token tiles of one weight panel are
+    // consecutive on one XCD, so the panel is read from HBM about once
     if (item < max_rtiles * ntn_r) {
-        const int mt = item / ntn_r;
-        wn = item % ntn_r;
-        if (mt >= total_rt) return;
-        int lo = 0, hi = nact - 1;  // last gi with s_tpre[gi] <= mt
+        const int gt = item / ntn_r;  // group gi owns items [ntn_r s_tpre[gi], ntn_r s_tpre[gi + 1])
+        if (gt >= total_rt) return;
+        int lo = 0, hi = nact - 1;  // last gi with s_tpre[gi] <= gt
         while (lo < hi) {
             const int mid = (lo + hi + 1) >> 1;
-            if (s_tpre[mid] <= mt) lo = mid;
+            if (s_tpre[mid] <= gt) lo = mid;
             else hi = mid - 1;
         }
         g = routed_group(a, s_list[lo], 2);
-        mt_local = mt - s_tpre[lo];
+        const int tg = s_tpre[lo + 1] - s_tpre[lo];
+        const int local = item - ntn_r * s_tpre[lo];
+        wn = local / tg;
+        mt_local = local % tg;
     } else {
         const int i2 = item - max_rtiles * ntn_r;
         const int tps = (a.T + kTn - 1) / kTn;
-        const int mt = i2 / ntn_s;
-        wn = i2 % ntn_s;
-        const int s = mt / tps;
+        const int s = i2 / (tps * ntn_s);
         if (s >= a.S) return;
         g = shared_group(a, s, 2);
-        mt_local = mt % tps;
+        const int local = i2 % (tps * ntn_s);
+        wn = local / tps;
+        mt_local = local % tps;
     }
     const int n0 = mt_local * kTn;
     if (n0 >= g.count) return;
@@ -478,6 +483,8 @@ __global__ void __launch_bounds__(256) k_ffn_tiled(Args a, int max_rtiles, int n
 #pragma unroll
         for (int j = 0; j < 4; ++j) acc[m][j] = f32x4{0.f, 0.f, 0.f, 0.f};
 
+    // one LDS buffer (so three workgroups fit on a CU); slab kt + 1 is loaded
+    // into registers while slab kt is multiplied out of LDS
     const int nk = K / kTk;
     u32x4 rw[4], rx[4];
     auto gload = [&](int kt) {
@@ -487,35 +494,29 @@ __global__ void __launch_bounds__(256) k_ffn_tiled(Args a, int max_rtiles, int n
             rx[i] = gX[i] ? *reinterpret_cast<const u32x4*>(gX[i] + kt * kTk) : u32x4{0u, 0u, 0u, 0u};
         }
     };
-    auto lstore = [&](int buf) {
+    gload(0);
+    for (int kt = 0; kt < nk; ++kt) {
 #pragma unroll
         for (int i = 0; i < 4; ++i) {
-            *reinterpret_cast<u32x4*>(&sW[buf][wb[i]][wl[i] * 8]) = rw[i];
-            *reinterpret_cast<u32x4*>(&sX[buf][cr[i]][cc[i]]) = rx[i];
+            *reinterpret_cast<u32x4*>(&sW[wb[i]][wl[i] * 8]) = rw[i];
+            *reinterpret_cast<u32x4*>(&sX[cr[i]][cc[i]]) = rx[i];
         }
-    };
-
-    gload(0);
-    lstore(0);
-    __syncthreads();
-    for (int kt = 0; kt < nk; ++kt) {
-        const int buf = kt & 1;
+        __syncthreads();
         if (kt + 1 < nk) gload(kt + 1);
 #pragma unroll
         for (int ks = 0; ks < kTk / 32; ++ks) {
             bf16x8 A[4], B[4];
 #pragma unroll
             for (int m = 0; m < 4; ++m)
-                A[m] = __builtin_bit_cast(bf16x8, *reinterpret_cast<const u32x4*>(&sW[buf][rtl_of[m] * 2 + ks][lane * 8]));
+                A[m] = __builtin_bit_cast(bf16x8, *reinterpret_cast<const u32x4*>(&sW[rtl_of[m] * 2 + ks][lane * 8]));
 #pragma unroll
             for (int j = 0; j < 4; ++j)
-                B[j] = __builtin_bit_cast(bf16x8, *reinterpret_cast<const u32x4*>(&sX[buf][64 * wc + 16 * j + r][ks * 32 + kq]));
+                B[j] = __builtin_bit_cast(bf16x8, *reinterpret_cast<const u32x4*>(&sX[64 * wc + 16 * j + r][ks * 32 + kq]));
 #pragma unroll
             for (int m = 0; m < 4; ++m)
 #pragma unroll
                 for (int j = 0; j < 4; ++j) acc[m][j] = mfma16x16x32(A[m], B[j], acc[m][j]);
         }
-        if (kt + 1 < nk) lstore(buf ^ 1);
         __syncthreads();
     }
 
