@@ -3,6 +3,7 @@
 // counting sort that repacks the (token, expert) pairs.
 #pragma once
 
+#include <limits.h>
 #include <math.h>
 
 #include "common.hpp"
@@ -14,18 +15,24 @@ constexpr int kFrontWaves = kFrontThreads / kWave;
 constexpr int kLgPitch = 257;                   // LDS row pitch of a score tile (E <= 256)
 constexpr int kScoreChunk = 64;                 // experts (4 MFMA row tiles) per reduction pass
 
-// Maximum over the wave: DPP within each row of 16 lanes, then the four row
-// maxima (every lane gets the result).  NaN inputs are ignored by fmaxf.
-__device__ __forceinline__ float wave_max(float v) {
-    v = fmaxf(v, __int_as_float(__builtin_amdgcn_mov_dpp(__float_as_int(v), 0xB1, 0xF, 0xF, false)));   // quad_perm 1,0,3,2
-    v = fmaxf(v, __int_as_float(__builtin_amdgcn_mov_dpp(__float_as_int(v), 0x4E, 0xF, 0xF, false)));   // quad_perm 2,3,0,1
-    v = fmaxf(v, __int_as_float(__builtin_amdgcn_mov_dpp(__float_as_int(v), 0x124, 0xF, 0xF, false)));  // row_ror 4
-    v = fmaxf(v, __int_as_float(__builtin_amdgcn_mov_dpp(__float_as_int(v), 0x128, 0xF, 0xF, false)));  // row_ror 8
-    const float r0 = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v), 0));
-    const float r1 = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v), 16));
-    const float r2 = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v), 32));
-    const float r3 = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v), 48));
-    return fmaxf(fmaxf(r0, r1), fmaxf(r2, r3));
+// Integer key with the order of the float scores: equal keys iff equal scores
+// (-0 is folded into +0), larger key iff larger score.
+__device__ __forceinline__ int score_key(float f) {
+    int b = __float_as_int(f);
+    if (b == (int)0x80000000) b = 0;
+    return b >= 0 ? b : (b ^ 0x7fffffff);
+}
+
+// Maximum over the wave: DPP within each row of 16 lanes (each step folds into
+// one v_max_i32 with a DPP operand), then the four row maxima on the scalar unit.
+__device__ __forceinline__ int wave_max_i32(int v) {
+    v = max(v, __builtin_amdgcn_mov_dpp(v, 0xB1, 0xF, 0xF, true));   // quad_perm 1,0,3,2
+    v = max(v, __builtin_amdgcn_mov_dpp(v, 0x4E, 0xF, 0xF, true));   // quad_perm 2,3,0,1
+    v = max(v, __builtin_amdgcn_mov_dpp(v, 0x124, 0xF, 0xF, true));  // row_ror 4
+    v = max(v, __builtin_amdgcn_mov_dpp(v, 0x128, 0xF, 0xF, true));  // row_ror 8
+    const int r0 = __builtin_amdgcn_readlane(v, 0), r1 = __builtin_amdgcn_readlane(v, 16);
+    const int r2 = __builtin_amdgcn_readlane(v, 32), r3 = __builtin_amdgcn_readlane(v, 48);
+    return max(max(r0, r1), max(r2, r3));
 }
 
 // LDS the top-k needs: selected (score, expert) of up to 64 rows x 8.
@@ -54,10 +61,11 @@ __device__ inline void topk_rank_block(const float* s_lg, int rows, int E, int k
         const int lane = lane_id(), nw = blockDim.x / kWave;
         for (int t = threadIdx.x / kWave; t < rows; t += nw) {
             const float v = (lane < E) ? s_lg[t * kLgPitch + lane] : 0.f;
+            const int key = score_key(v);
             bool open = lane < E;
             for (int j = 0; j < k; ++j) {
-                const float m = wave_max(open ? v : -INFINITY);
-                const unsigned long long cand = __ballot(open && v == m);
+                const int m = wave_max_i32(open ? key : INT_MIN);
+                const unsigned long long cand = __ballot(open && key == m);  // never empty: k <= E
                 const int e = cand ? __ffsll((long long)cand) - 1 : -1;
                 if (lane == e) open = false;
                 if (lane == 0 && e >= 0) {
