@@ -13,7 +13,9 @@ Prints one JSON line on stdout:
 * value: tokens per second of the whole layer forward;
 * roofline: the dominant kernel (FFN phase 1: gate/up projections + SwiGLU),
   its algorithmic bytes per launch / its mean duration from HIP events recorded
-  by the library around that kernel on the launch stream, against 8 TB/s;
+  by the library around that kernel on the launch stream, against 8 TB/s (decode
+  batches); for prefill-size batches (more than 64 tokens) its algorithmic
+  FLOPs per launch / the same duration, against 2.5 PFLOP/s dense bf16;
 * cpu_baseline: the CPU oracle timed on this host on the same workload.
 """
 from __future__ import annotations
@@ -33,7 +35,7 @@ sys.path.insert(0, ROOT)
 HBM_PEAK_GBPS = 8000.0          # MI355X HBM3E, 8 TB/s
 MFMA_BF16_PEAK_TFLOPS = 2500.0  # dense bf16
 METRIC = "MoE-layer tokens/sec + achieved HBM GB/s (expert weights) at decode batch"
-TRAFFIC_FILE = os.path.join(ROOT, "profiles", "traffic_ffn_phase1_c2_mixtral_decode.txt")
+TRAFFIC_DIR = os.path.join(ROOT, "profiles")
 KERNEL_SOURCES = [os.path.join(ROOT, "paper_2608_21614_amd", "csrc", n) for n in ("ffn.hip", "common.hpp")]
 STAGES = ["route_topk", "repack", "offload_pack", "ffn_phase1", "ffn_phase2", "combine"]
 
@@ -52,10 +54,11 @@ def kernel_source_hash() -> str:
 
 def read_traffic(workload: str):
     """HBM bytes per launch of the dominant kernel from committed counter runs, or None if stale/missing."""
-    if not os.path.exists(TRAFFIC_FILE):
+    path = os.path.join(TRAFFIC_DIR, f"traffic_ffn_phase1_{workload}.txt")
+    if not os.path.exists(path):
         return None
     kv = {}
-    for line in open(TRAFFIC_FILE):
+    for line in open(path):
         m = re.match(r"^([a-z_]+):\s*(\S+)", line.strip())
         if m:
             kv[m.group(1)] = m.group(2)
@@ -215,8 +218,22 @@ def main() -> int:
     tokens_per_s = cfg.tokens / (ms_per_step * 1e-3)
     p1_us = float(p1_ms.mean() * 1e3)
     p1_s = p1_us * 1e-6
-    achieved = alg["phase1_bytes"] / p1_s / 1e9
     traffic = read_traffic(args.workload)
+    if cfg.tokens > 64:
+        # prefill-size batches run the tiled MFMA kernels, at the ridge: FLOP rate
+        # against the dense bf16 matrix-core peak
+        achieved = alg["phase1_flops"] / p1_s / 1e12
+        roofline = {"kernel": "k_ffn_tiled (phase 1: gate/up projections + SwiGLU)", "bound": "mfma",
+                    "achieved": achieved, "peak": MFMA_BF16_PEAK_TFLOPS, "unit": "TFLOP/s",
+                    "frac": achieved / MFMA_BF16_PEAK_TFLOPS, "traffic": traffic,
+                    "algorithmic_flops_per_launch": alg["phase1_flops"],
+                    "algorithmic_bytes_per_launch": alg["phase1_bytes"],
+                    "hbm_frac_algorithmic": alg["phase1_bytes"] / p1_s / 1e9 / HBM_PEAK_GBPS, "mean_launch_us": p1_us}
+    else:
+        achieved = alg["phase1_bytes"] / p1_s / 1e9
+        roofline = {"kernel": "k_ffn_stream (phase 1: gate/up projections + SwiGLU)", "bound": "hbm",
+                    "achieved": achieved, "peak": HBM_PEAK_GBPS, "unit": "GB/s", "frac": achieved / HBM_PEAK_GBPS,
+                    "traffic": traffic, "algorithmic_bytes_per_launch": alg["phase1_bytes"], "mean_launch_us": p1_us}
     result = {
         "metric": METRIC,
         "value": tokens_per_s,
@@ -229,7 +246,7 @@ def main() -> int:
         "scaling": "weak",
         "vs_baseline": None,
         "dtype": "bf16" if cfg.dtype == "bf16" else "f32",
-        "data": "synthetic (seeded: x ~ N(0,1), weights ~ N(0,0.02^2), bf16)",
+        "data": f"synthetic (seeded: x ~ N(0,1), weights ~ N(0,0.02^2), {cfg.dtype})",
         "config": {"workload": args.workload, "description": cfg.description, "tokens": cfg.tokens,
                    "hidden": cfg.hidden, "experts": cfg.experts, "ffn": cfg.ffn, "top_k": cfg.top_k,
                    "shared": cfg.shared, "shared_ffn": cfg.shared_ffn, "resident_slots": dev.slots,
@@ -240,17 +257,8 @@ def main() -> int:
         "hbm_gbps_layer_algorithmic": alg["layer_bytes"] / (ms_per_step * 1e-3) / 1e9,
         "stages_us_instrumented": stage_us,
         "ms_per_step_without_events": ms_no_events,
-        "roofline": {
-            "kernel": "k_ffn_stream (phase 1: gate/up projections + SwiGLU)",
-            "bound": "hbm",
-            "achieved": achieved,
-            "peak": HBM_PEAK_GBPS,
-            "unit": "GB/s",
-            "frac": achieved / HBM_PEAK_GBPS,
-            "traffic": traffic,
-            "algorithmic_bytes_per_launch": alg["phase1_bytes"],
-            "mean_launch_us": p1_us,
-        },
+        "mfma_tflops_layer_algorithmic": alg["flops"] / (ms_per_step * 1e-3) / 1e12,
+        "roofline": roofline,
     }
     if not args.no_cpu_baseline:
         log("[bench] timing the CPU oracle")
