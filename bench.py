@@ -128,9 +128,15 @@ def main() -> int:
 
     import paper_2608_21614_amd as moe
     from paper_2608_21614_amd.device import DeviceLayer, to_host
-    from workloads import CONFIGS, SyntheticLayer
+    from workloads import CONFIGS, TRACE, SyntheticLayer
 
-    cfg = CONFIGS[args.workload]
+    # the stage-structured trace's layer shape is timed as one layer call (no stage bias)
+    cfgs = dict(CONFIGS)
+    cfgs[TRACE.name] = TRACE.layer_config()
+    if args.workload not in cfgs:
+        print(json.dumps({"error": f"unknown workload {args.workload}; one of {sorted(cfgs)}"}), flush=True)
+        return 2
+    cfg = cfgs[args.workload]
     torch.cuda.set_device(0)
     log(f"[bench] generating {args.workload} seed {args.seed}")
     layer = SyntheticLayer(cfg, args.seed)

@@ -162,7 +162,10 @@ class TraceConfig:
         return MoEConfig(self.name, self.dtype, tokens=self.batch, hidden=self.hidden,
                          experts=self.experts, ffn=self.ffn, top_k=self.top_k,
                          n_resident=self.n_slots, residency="random", bias="none",
-                         x_std=self.x_std, w_std=self.w_std)
+                         x_std=self.x_std, w_std=self.w_std,
+                         description=f"one layer call of the stage trace: {self.dtype} decode batch of {self.batch} "
+                                     f"tokens, H {self.hidden}, {self.experts} experts F {self.ffn}, top-{self.top_k}, "
+                                     f"{self.n_slots}/{self.experts} resident")
 
     def logit_std(self) -> float:
         return self.x_std * self.w_std * math.sqrt(self.hidden)
