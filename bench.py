@@ -103,6 +103,38 @@ def cpu_baseline(layer, seconds: float):
                       f"router + repack, fp64 C with OpenMP), {el:.1f} s"}
 
 
+def hybrid_timings(layer, dev, n: int, threads: int):
+    """Median timings of n hybrid calls: GPU resident/shared experts, host offloaded experts, merge."""
+    import numpy as np
+    import torch
+    from paper_2608_21614_amd.hybrid import HybridLayer
+    log(f"[bench] hybrid: {n} calls, {threads} host threads")
+    hy = HybridLayer(dev, layer.w13, layer.w2, threads=threads)
+    for _ in range(2):
+        hy.forward()
+        torch.cuda.synchronize()
+    rows = []
+    for _ in range(n):
+        hy.forward()
+        torch.cuda.synchronize()
+        rows.append(hy.timings())
+    med = {k: float(np.median([r[k] for r in rows])) for k in rows[0] if k != "host_t0"}
+    c = layer.cfg
+    b = 2 if c.dtype == "bf16" else 4
+    n_off_experts = int(sum(1 for e in range(c.experts) if not layer.resident[e] and
+                            (to_host_counts(hy)[e] > 0)))
+    host_bytes = n_off_experts * 3 * c.hidden * c.ffn * b
+    med["offloaded_experts"] = n_off_experts
+    med["host_weight_bytes"] = host_bytes
+    med["host_ffn_GBps"] = host_bytes / (med["host_ffn_ms"] * 1e-3) / 1e9 if med["host_ffn_ms"] > 0 else None
+    med["threads"] = threads
+    return med
+
+
+def to_host_counts(hy):
+    return hy.h_counts.numpy()
+
+
 def main() -> int:
     ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
     ap.add_argument("--gpus", type=int, default=1)
@@ -113,6 +145,10 @@ def main() -> int:
     ap.add_argument("--copies", type=int, default=4, help="rotated expert-weight copies")
     ap.add_argument("--cpu-seconds", type=float, default=10.0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--hybrid", type=int, default=0, metavar="N",
+                    help="also time N hybrid layer calls (offloaded experts on the host, Section IV-D.2); "
+                         "reported as an extra object, `value` stays the GPU path")
+    ap.add_argument("--host-threads", type=int, default=16)
     ap.add_argument("--calib-copy-mib", type=int, default=0,
                     help="run one plain device copy of this many MiB first (counter calibration)")
     args = ap.parse_args()
@@ -266,6 +302,8 @@ def main() -> int:
         "mfma_tflops_layer_algorithmic": alg["flops"] / (ms_per_step * 1e-3) / 1e12,
         "roofline": roofline,
     }
+    if args.hybrid > 0:
+        result["hybrid"] = hybrid_timings(layer, dev, args.hybrid, args.host_threads)
     if not args.no_cpu_baseline:
         log("[bench] timing the CPU oracle")
         result["cpu_baseline"] = cpu_baseline(layer, args.cpu_seconds)

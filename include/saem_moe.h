@@ -17,8 +17,9 @@
  *
  * Conventions for every call
  *   - Returns moe_status.  No exception or abort crosses the ABI.
- *   - All tensor pointers are DEVICE pointers owned by the caller.  The library
- *     never allocates or frees device memory and never synchronises the stream.
+ *   - All tensor pointers are DEVICE pointers owned by the caller (except for
+ *     the host-side calls moe_stage_plan and moe_host_ffn).  The library never
+ *     allocates or frees device memory and never synchronises the stream.
  *   - Work is enqueued on `stream` (a hipStream_t; NULL is the null stream).
  *   - Arguments are validated on the host before anything is enqueued; a call
  *     that returns an error has enqueued nothing.  Validation never touches
@@ -250,6 +251,36 @@ moe_status moe_stage_accumulate(int32_t experts, const int32_t* counts, int64_t*
  */
 moe_status moe_stage_plan(int32_t experts, int32_t slots, const int64_t* log, const int32_t* prev_slot,
                           int32_t* new_slot);
+
+/* flags of moe_host_ffn */
+#define MOE_HOST_PIN 1u    /* pin the worker threads to the calling thread's CPUs on one NUMA node */
+
+/*
+ * In-situ host execution of the offloaded experts (Section IV-D.1, IV-D.2):
+ * the SwiGLU of every offloaded expert over its rows of the packed offloaded
+ * list, on the CPU, in parallel over output features, by `threads` worker
+ * threads (<= 0: one per available CPU; with MOE_HOST_PIN, one per CPU of the
+ * NUMA node).  The result is the y_off that moe_combine merges (the merge step
+ * of Section IV-D.2).  Everything here is HOST memory; no device work.
+ *   dims               the layer's shapes (dtype = dtype of the weights and rows)
+ *   counts, seg_start  [E] int32, host copies of moe_repack's outputs
+ *   n_res              host copy of moe_repack's n_res
+ *   w13[e], w2[e]      host pointers, for every expert e with offloaded rows
+ *                      (counts[e] > 0 and seg_start[e] >= n_res; others may be
+ *                      NULL): ROW-MAJOR [2F, H] (rows 0..F-1 = W1, F..2F-1 =
+ *                      W3) and [H, F] of dims.dtype, the matrices
+ *                      moe_pack_weights takes for the device slots
+ *   off_rows           [T*k - n_res, H] dims.dtype, host copy of the packed
+ *                      offloaded rows (moe_repack / moe_layer_forward off_rows)
+ *   y_off              [T*k - n_res, H] fp32 out: y_off[r] = SwiGLU_e(off_rows[r])
+ *                      for the expert e that owns packed row n_res + r
+ * fp32 accumulation; A = silu(x W1) * (x W3) is kept in fp32.  Returns
+ * MOE_ERR_INVALID_ARG if the offloaded segments do not tile [n_res, T*k) or a
+ * needed pointer is NULL; nothing is written then.
+ */
+moe_status moe_host_ffn(const moe_dims* dims, const int32_t* counts, const int32_t* seg_start, int32_t n_res,
+                        const void* const* w13, const void* const* w2, const void* off_rows, float* y_off,
+                        int32_t threads, uint32_t flags);
 
 #ifdef __cplusplus
 }

@@ -21,11 +21,12 @@ MOE_OK, MOE_ERR_INVALID_ARG, MOE_ERR_UNSUPPORTED, MOE_ERR_WORKSPACE, MOE_ERR_HIP
 MOE_F32, MOE_BF16 = 0, 1
 MOE_LOGITS_IN = 1
 MOE_STAGE_EVENTS = 7
+MOE_HOST_PIN = 1
 
 EXPORTED = [
     "moe_abi_version", "moe_status_str", "moe_check_dims", "moe_workspace_bytes", "moe_route_topk",
     "moe_repack", "moe_grouped_ffn", "moe_combine", "moe_layer_forward", "moe_stage_accumulate",
-    "moe_stage_plan", "moe_pack_weights",
+    "moe_stage_plan", "moe_pack_weights", "moe_host_ffn",
 ]
 
 
@@ -99,6 +100,8 @@ def _load() -> ctypes.CDLL:
         "moe_stage_accumulate": ([i32, _vp, _vp, _vp], ctypes.c_int),
         "moe_stage_plan": ([i32, i32, _vp, _vp, _vp], ctypes.c_int),
         "moe_pack_weights": ([_vp, _vp, ctypes.c_int64, ctypes.c_int64, i32, _vp], ctypes.c_int),
+        "moe_host_ffn": ([D, _vp, _vp, i32, ctypes.POINTER(_vp), ctypes.POINTER(_vp), _vp, _vp, i32, u32],
+                         ctypes.c_int),
     }
     for name, (args, res) in sig.items():
         fn = getattr(lib, name)
@@ -206,6 +209,40 @@ def moe_pack_weights(src, dst, stream=None):
 
 def moe_stage_accumulate(experts: int, counts, log, stream=None):
     _check(lib.moe_stage_accumulate(int(experts), _p(counts), _p(log), _stream(stream)), "moe_stage_accumulate")
+
+
+def moe_host_ffn(dims, counts, seg_start, n_res: int, w13_host, w2_host, off_rows, y_off=None, threads: int = 0,
+                 pin: bool = False):
+    """Host execution of the offloaded experts (host numpy arrays only).
+
+    counts, seg_start: int32 [E]; w13_host[e] / w2_host[e]: row-major [2F, H] / [H, F]
+    arrays of the layer dtype (uint16 bf16 bits or float32) for the experts with
+    offloaded rows, None for the others; off_rows: [T*k - n_res, H].  Returns
+    y_off [T*k - n_res, H] float32 (written into `y_off` when given).
+    """
+    import numpy as np
+    E, H = dims.experts, dims.hidden
+    cnt = np.ascontiguousarray(counts, dtype=np.int32)
+    seg = np.ascontiguousarray(seg_start, dtype=np.int32)
+    want = np.uint16 if dims.dtype == MOE_BF16 else np.float32
+    n_off = dims.tokens * dims.top_k - int(n_res)
+    rows = np.ascontiguousarray(off_rows, dtype=want) if n_off > 0 else None
+    if y_off is None:
+        y_off = np.empty((max(n_off, 0), H), dtype=np.float32)
+    keep = []  # keeps the contiguous weight arrays alive for the call
+    p13 = (_vp * E)()
+    p2 = (_vp * E)()
+    for e in range(E):
+        if w13_host[e] is not None:
+            a = np.ascontiguousarray(w13_host[e], dtype=want)
+            b = np.ascontiguousarray(w2_host[e], dtype=want)
+            keep += [a, b]
+            p13[e], p2[e] = a.ctypes.data, b.ctypes.data
+    _check(lib.moe_host_ffn(ctypes.byref(dims), cnt.ctypes.data, seg.ctypes.data, int(n_res), p13, p2,
+                            rows.ctypes.data if rows is not None else None,
+                            y_off.ctypes.data if n_off > 0 else None, int(threads),
+                            MOE_HOST_PIN if pin else 0), "moe_host_ffn")
+    return y_off
 
 
 def moe_stage_plan(log_host, prev_slot_host, slots: int):

@@ -15,6 +15,7 @@ CSRC = os.path.join(HERE, "csrc")
 LIB = os.path.join(HERE, "libsaem_moe.so")
 BUILD_DIR = os.path.join(HERE, "_build")
 SOURCES = ["abi.hip", "route.hip", "repack.hip", "ffn.hip", "combine.hip", "pack.hip"]
+HOST_SOURCES = ["host_ffn.cpp"]   # host-only C++ (system compiler)
 ARCH = "gfx950"
 
 HIPCC_FLAGS = [
@@ -47,10 +48,20 @@ def build(verbose: bool = False) -> str:
             sys.stderr.write(r.stderr)
         return obj
 
-    with ThreadPoolExecutor(len(SOURCES)) as ex:
-        objs = list(ex.map(compile_one, SOURCES))
+    def compile_host(src: str) -> str:
+        obj = os.path.join(BUILD_DIR, src.replace(".cpp", ".o"))
+        cmd = [shutil.which("g++") or "g++", "-O3", "-std=c++17", "-fPIC", "-pthread", "-Wall", *inc, "-c",
+               os.path.join(CSRC, src), "-o", obj]
+        r = subprocess.run(cmd, capture_output=True, text=True)
+        if r.returncode != 0:
+            raise RuntimeError(f"g++ failed on {src}:\n{r.stderr}")
+        return obj
+
+    with ThreadPoolExecutor(len(SOURCES) + len(HOST_SOURCES)) as ex:
+        futs = [ex.submit(compile_one, s) for s in SOURCES] + [ex.submit(compile_host, s) for s in HOST_SOURCES]
+        objs = [f.result() for f in futs]
     tmp = LIB + ".tmp"
-    cmd = [hipcc, f"--offload-arch={ARCH}", "-shared", "-fPIC", "-o", tmp, *objs]
+    cmd = [hipcc, f"--offload-arch={ARCH}", "-shared", "-fPIC", "-pthread", "-o", tmp, *objs]
     r = subprocess.run(cmd, capture_output=True, text=True)
     if r.returncode != 0:
         raise RuntimeError(f"link failed:\n{r.stderr}")

@@ -1,0 +1,126 @@
+"""In-situ host execution of the offloaded experts (moe_host_ffn, SAEM Section IV-D).
+
+Host-only calls of the library: no GPU needed.  The offloaded list is built
+from the oracle's own routing and repacking (the rows the GPU would pack), and
+every host result row is compared with the oracle's fp64 SwiGLU of that row's
+expert.  Inputs are exact bf16/fp32 values and the host accumulates in fp32
+without rounding A, so the bar is the fp32 one (rel-L2 <= 1e-5) for both dtypes.
+"""
+from dataclasses import replace
+
+import numpy as np
+import pytest
+
+import oracle
+from workloads import CONFIGS, SyntheticLayer
+
+moe = pytest.importorskip("paper_2608_21614_amd")
+
+TOL = 1e-5
+
+
+def rel_l2(a, b):
+    a = np.asarray(a, dtype=np.float64)
+    b = np.asarray(b, dtype=np.float64)
+    return float(np.linalg.norm(a - b) / max(np.linalg.norm(b), 1e-300))
+
+
+def offloaded_case(cfg, seed):
+    L = SyntheticLayer(cfg, seed)
+    lg = oracle.router_logits(L.x, L.w_router, L.bias)
+    idx, _ = oracle.topk(lg, cfg.top_k)
+    rp = oracle.repack(idx, L.resident)
+    n_res = int(rp["n_res"])
+    P = cfg.tokens * cfg.top_k
+    rows_tok = rp["perm"][n_res:P] // cfg.top_k
+    off_rows = L.x[rows_tok]
+    w13 = [L.w13(e) if not L.resident[e] else None for e in range(cfg.experts)]
+    w2 = [L.w2(e) if not L.resident[e] else None for e in range(cfg.experts)]
+    dims = moe.make_dims(cfg.tokens, cfg.hidden, cfg.experts, cfg.ffn, cfg.top_k, 0, 0,
+                         slots=int(L.resident.sum()), dtype=moe.MOE_BF16 if cfg.dtype == "bf16" else moe.MOE_F32)
+    return L, rp, n_res, off_rows, w13, w2, dims
+
+
+def expected(L, rp, n_res, cfg):
+    """oracle SwiGLU of every offloaded row, expert by expert (fp64)."""
+    P = cfg.tokens * cfg.top_k
+    out = np.zeros((P - n_res, cfg.hidden))
+    for e in range(cfg.experts):
+        c, s = int(rp["counts"][e]), int(rp["seg_start"][e])
+        if L.resident[e] or c == 0:
+            continue
+        toks = rp["perm"][s:s + c] // cfg.top_k
+        out[s - n_res:s - n_res + c] = oracle.expert_ffn(L.x, toks, L.w13(e), L.w2(e))
+    return out
+
+
+SMALL = [
+    # name, dtype, tokens, hidden, experts, ffn, top_k
+    ("bf16_24x256", "bf16", 24, 256, 8, 192, 2),
+    ("f32_16x128", "f32", 16, 128, 8, 128, 2),
+    ("bf16_40x128_k4", "bf16", 40, 128, 6, 64, 4),   # experts with > 8 rows: several row blocks
+]
+
+
+@pytest.mark.parametrize("name,dtype,T,H,E,F,k", SMALL, ids=[c[0] for c in SMALL])
+@pytest.mark.parametrize("seed", [0, 1])
+def test_host_ffn_matches_oracle(name, dtype, T, H, E, F, k, seed):
+    cfg = replace(CONFIGS["c2_mixtral_decode"], name=name, dtype=dtype, tokens=T, hidden=H, experts=E, ffn=F,
+                  top_k=k, n_resident=E // 2)
+    L, rp, n_res, off_rows, w13, w2, dims = offloaded_case(cfg, seed)
+    assert T * k - n_res > 0
+    y = moe.moe_host_ffn(dims, rp["counts"], rp["seg_start"], n_res, w13, w2, off_rows)
+    ref = expected(L, rp, n_res, cfg)
+    assert y.shape == ref.shape
+    assert rel_l2(y, ref) <= TOL
+    # every row on its own too (no row may be skipped or swapped)
+    for r in range(ref.shape[0]):
+        assert rel_l2(y[r], ref[r]) <= 10 * TOL, r
+
+
+def test_host_ffn_thread_count_and_pinning_do_not_change_bits():
+    cfg = replace(CONFIGS["c2_mixtral_decode"], name="t", tokens=24, hidden=256, experts=8, ffn=192, top_k=2,
+                  n_resident=3)
+    L, rp, n_res, off_rows, w13, w2, dims = offloaded_case(cfg, 5)
+    y1 = moe.moe_host_ffn(dims, rp["counts"], rp["seg_start"], n_res, w13, w2, off_rows, threads=1)
+    y7 = moe.moe_host_ffn(dims, rp["counts"], rp["seg_start"], n_res, w13, w2, off_rows, threads=7)
+    yp = moe.moe_host_ffn(dims, rp["counts"], rp["seg_start"], n_res, w13, w2, off_rows, pin=True)
+    assert np.array_equal(y1, y7) and np.array_equal(y1, yp)
+
+
+def test_host_ffn_all_resident_is_a_no_op():
+    cfg = replace(CONFIGS["c2_mixtral_decode"], name="t", tokens=8, hidden=128, experts=4, ffn=64, top_k=2,
+                  n_resident=4)
+    L, rp, n_res, off_rows, w13, w2, dims = offloaded_case(cfg, 0)
+    assert n_res == 16
+    y = moe.moe_host_ffn(dims, rp["counts"], rp["seg_start"], n_res, [None] * 4, [None] * 4, off_rows)
+    assert y.shape == (0, 128)
+
+
+def test_host_ffn_rejects_inconsistent_lists():
+    cfg = replace(CONFIGS["c2_mixtral_decode"], name="t", tokens=16, hidden=128, experts=8, ffn=64, top_k=2,
+                  n_resident=4)
+    L, rp, n_res, off_rows, w13, w2, dims = offloaded_case(cfg, 2)
+    off = [e for e in range(8) if not L.resident[e] and rp["counts"][e] > 0]
+    assert len(off) >= 2
+    # a missing weight pointer for an expert that has offloaded rows
+    w13_bad = list(w13)
+    w13_bad[off[0]] = None
+    with pytest.raises(moe.MoeError):
+        moe.moe_host_ffn(dims, rp["counts"], rp["seg_start"], n_res, w13_bad, w2, off_rows)
+    # overlapping segments
+    seg = rp["seg_start"].copy()
+    seg[off[1]] = seg[off[0]]
+    with pytest.raises(moe.MoeError):
+        moe.moe_host_ffn(dims, rp["counts"], seg, n_res, w13, w2, off_rows)
+    # segments that do not cover the offloaded list
+    cnt = rp["counts"].copy()
+    cnt[off[0]] -= 1
+    with pytest.raises(moe.MoeError):
+        moe.moe_host_ffn(dims, cnt, rp["seg_start"], n_res, w13, w2, off_rows)
+    # n_res outside [0, T*k]
+    with pytest.raises(moe.MoeError):
+        moe.moe_host_ffn(dims, rp["counts"], rp["seg_start"], 16 * 2 + 1, w13, w2, off_rows)
+    # unknown flag bits
+    st = moe.lib.moe_host_ffn(moe.ctypes.byref(dims), None, None, 0, None, None, None, None, 0, 2)
+    assert st == moe.MOE_ERR_INVALID_ARG
