@@ -157,25 +157,32 @@ std::vector<int> local_cpus() {
     return allowed;
 }
 
-// Runs fn(item) for item in [0, n_items) on `nthreads` threads (the caller is
-// one of them), workers pinned to `cpus` when given.  Items are taken in order
-// from an atomic counter.
+// Runs fn(item) for item in [0, n_items) on `nthreads` threads, items taken in
+// order from an atomic counter.  Unpinned, the caller is one of the threads.
+// Pinned (cpus given), all `nthreads` are new threads, worker i on cpus[i % n],
+// and the caller only waits: its own affinity is never changed.
 template <typename Fn>
 void parallel_items(int n_items, int nthreads, const std::vector<int>& cpus, Fn fn) {
     std::atomic<int> next{0};
-    auto worker = [&](int id) {
-        if (!cpus.empty()) {
-            cpu_set_t one;
-            CPU_ZERO(&one);
-            CPU_SET(cpus[id % cpus.size()], &one);
-            pthread_setaffinity_np(pthread_self(), sizeof(one), &one);
-        }
+    auto work = [&]() {
         for (int i = next.fetch_add(1); i < n_items; i = next.fetch_add(1)) fn(i);
     };
     std::vector<std::thread> pool;
-    pool.reserve(nthreads > 1 ? nthreads - 1 : 0);
-    for (int t = 1; t < nthreads; ++t) pool.emplace_back(worker, t);
-    worker(0);
+    if (cpus.empty()) {
+        pool.reserve(nthreads > 1 ? nthreads - 1 : 0);
+        for (int t = 1; t < nthreads; ++t) pool.emplace_back(work);
+        work();
+    } else {
+        pool.reserve(nthreads);
+        for (int t = 0; t < nthreads; ++t)
+            pool.emplace_back([&, t]() {
+                cpu_set_t one;
+                CPU_ZERO(&one);
+                CPU_SET(cpus[t % cpus.size()], &one);
+                pthread_setaffinity_np(pthread_self(), sizeof(one), &one);
+                work();
+            });
+    }
     for (auto& th : pool) th.join();
 }
 

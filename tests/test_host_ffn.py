@@ -124,3 +124,17 @@ def test_host_ffn_rejects_inconsistent_lists():
     # unknown flag bits
     st = moe.lib.moe_host_ffn(moe.ctypes.byref(dims), None, None, 0, None, None, None, None, 0, 2)
     assert st == moe.MOE_ERR_INVALID_ARG
+
+
+def test_host_ffn_pinning_leaves_the_callers_affinity_alone():
+    """Pinned workers are new threads: the calling thread keeps its CPU set, so the next
+    call still spreads its workers over the whole node (regression: the caller pinned
+    itself to one CPU, and later calls then pinned every worker to that CPU)."""
+    import os
+    cfg = replace(CONFIGS["c2_mixtral_decode"], name="t", tokens=16, hidden=128, experts=8, ffn=64, top_k=2,
+                  n_resident=4)
+    L, rp, n_res, off_rows, w13, w2, dims = offloaded_case(cfg, 4)
+    before = os.sched_getaffinity(0)
+    for _ in range(2):
+        moe.moe_host_ffn(dims, rp["counts"], rp["seg_start"], n_res, w13, w2, off_rows, threads=4, pin=True)
+    assert os.sched_getaffinity(0) == before
