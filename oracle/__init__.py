@@ -337,8 +337,8 @@ def cache_hit_ratio(counts: np.ndarray, resident: np.ndarray) -> float:
     return float((c * r).sum()) / tot if tot else 1.0
 
 
-def stage_replay(counts: np.ndarray, stage_len: np.ndarray, initial_slot: np.ndarray, n_slots: int):
-    """Stage-aware residency over a decode trace (Sections IV-B.2, IV-C.2, V-C).
+def stage_replay(counts: np.ndarray, stage_len: np.ndarray, initial_slot: np.ndarray, n_slots: int, lag: int = 0):
+    """Stage-aware residency over a decode trace (Sections IV-B.2, IV-C.2, IV-C.3, V-C).
 
     counts[step, layer, e]: routed pairs per expert of each (step, layer) call;
     routing does not depend on where experts live, so the counts are fixed
@@ -351,6 +351,13 @@ def stage_replay(counts: np.ndarray, stage_len: np.ndarray, initial_slot: np.nda
     planned from its own log.  CHR = resident pairs / all pairs; eta_CHR is their
     ratio (Eq. upper_bound).
 
+    lag (online policy only): the weights of experts that enter the resident set
+    at a boundary are copied to the GPU while the next stage's first steps run
+    (Section IV-C.3); for the first ``lag`` steps of every stage after the first,
+    only the experts that keep their slot are resident (the evicted ones' slots
+    are being overwritten, the incoming ones are still in flight).  lag = 0: the
+    new residency holds from the stage's first step.
+
     Returns slot_history [n_stages, layers, E] (the slots in effect during each
     stage), resident [steps, layers, E], chr_online, chr_clairvoyant, eta_chr.
     """
@@ -362,12 +369,17 @@ def stage_replay(counts: np.ndarray, stage_len: np.ndarray, initial_slot: np.nda
     hist = np.empty((len(stage_len), layers, E), dtype=np.int32)
     resident = np.empty((steps, layers, E), dtype=bool)
     hit_on = hit_cv = 0
+    prev_res = None
     for s, (a, b) in enumerate(zip(starts, ends)):
         hist[s] = slot
         res = (slot >= 0) & (slot < n_slots)
         resident[a:b] = res[None]
+        if s > 0 and lag > 0:
+            stay = res & prev_res & (slot == hist[s - 1])    # kept its slot across the boundary
+            resident[a:min(a + lag, b)] = stay[None]
         log = c[a:b].sum(axis=0)                     # [layers, E]
-        hit_on += int((log * res).sum())
+        hit_on += int((c[a:b] * resident[a:b]).sum())
+        prev_res = res
         for l in range(layers):
             own = stage_plan(log[l], n_slots, np.full(E, -1, np.int32))
             hit_cv += int(log[l][(own >= 0)].sum())

@@ -462,3 +462,28 @@ def test_stage_replay_stable_routing_and_exact_ratio():
     assert r["chr_online"] == (2 * 5 + 10 * 8) / (12 * 8)
     assert r["chr_clairvoyant"] == 1.0
     assert r["resident"][1:].all(axis=0)[:, [1, 3]].all()
+
+
+def test_stage_replay_prefetch_lag_hand_trace():
+    """Copies overlapped with the next stage's first steps (Section IV-C.3): during the first
+    `lag` steps of a stage only the experts that keep their slot are resident."""
+    c = np.zeros((8, 1, 4), int)
+    c[0:2, 0] = [3, 1, 0, 0]          # stage 0 (2 steps): log [6, 2, 0, 0] -> keep {0, 1}
+    c[2:5, 0] = [0, 2, 2, 0]          # stage 1 (3 steps): log [0, 6, 6, 0] -> {1 stays, 2 enters slot 0}
+    c[5:8, 0] = [0, 0, 1, 5]          # stage 2 (3 steps)
+    init = np.array([[0, 1, -1, -1]])
+    lens = np.array([2, 3, 3])
+    r0 = oracle.stage_replay(c, lens, init, 2)
+    assert r0["slot_history"][2].tolist() == [[-1, 1, 0, -1]]
+    assert r0["chr_online"] == (8 + 6 + 3) / 38
+    r2 = oracle.stage_replay(c, lens, init, 2, lag=2)
+    assert r2["chr_online"] == (8 + 6 + 1) / 38
+    assert r2["resident"][5, 0].tolist() == [False, True, False, False]
+    assert r2["resident"][6, 0].tolist() == [False, True, False, False]
+    assert r2["resident"][7, 0].tolist() == [False, True, True, False]
+    # stage 1 keeps stage 0's map: the lag changes nothing there
+    assert (r2["resident"][2:5] == r0["resident"][2:5]).all()
+    # a lag longer than the stage: the incoming expert never serves a pair in it
+    r9 = oracle.stage_replay(c, lens, init, 2, lag=9)
+    assert r9["chr_online"] == (8 + 6 + 0) / 38
+    assert r9["chr_clairvoyant"] == r0["chr_clairvoyant"]
