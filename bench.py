@@ -131,6 +131,49 @@ def hybrid_timings(layer, dev, n: int, threads: int):
     return med
 
 
+def trace_timings(seed: int, lags):
+    """The stage-structured decode trace with real slot copies (Section IV-C), per prefetch lag.
+
+    Routers, stage biases and per-call activations are the trace's own (so the
+    residency trajectory and CHR are the ones the parity tests check); every
+    (layer, expert) gets its own pinned host buffer filled with one seeded
+    expert's weights -- the values do not change routing, copies or kernel time.
+    """
+    import numpy as np
+    import torch
+    from paper_2608_21614_amd.device import to_device
+    from paper_2608_21614_amd.residency import StageResidencyRunner
+    from workloads import TRACE, StageTrace
+    c = TRACE
+    trace = StageTrace(c, seed=seed)
+    L, E = c.layers, c.experts
+    layers = [trace.layer(l, cache_weights=False) for l in range(L)]
+    log(f"[bench] trace: {c.steps} steps x {L} layers, {trace.n_stages} stages; generating inputs")
+    xs = []
+    for l in range(L):
+        xs.append(to_device(np.stack([trace.x(s, l) for s in range(c.steps)])))   # [steps, T, H] on the device
+    base13, base2 = layers[0].w13(0), layers[0].w2(0)
+    out = {"steps": c.steps, "layers": L, "stages": int(trace.n_stages), "batch": c.batch, "slots": c.n_slots,
+           "weights": "one seeded expert's weights in every (layer, expert) host buffer", "runs": []}
+    runner = None
+    for lag in lags:
+        log(f"[bench] trace run, prefetch lag {lag}")
+        if runner is None:
+            runner = StageResidencyRunner(trace, [lay.w_router for lay in layers], lambda l, e: (base13, base2),
+                                          lambda s, l: xs[l][s], lag=lag)
+            runner.prepare_host_weights()
+        else:   # same host buffers and slot pools, fresh trajectory
+            runner.reset(lag)
+        r = runner.run()
+        calls = r["calls"]
+        out["runs"].append({"lag": lag, "trace_ms": r["trace_ms"], "us_per_layer_call": r["trace_ms"] * 1e3 / calls,
+                            "chr_online": r["chr_online"], "copied_experts": r["copied_experts"],
+                            "copy_ms_total": r["copy_ms_total"], "copy_GBps": r["copy_GBps"],
+                            "stall_ms_total": r["stall_ms_total"]})
+        log(f"[bench]   {out['runs'][-1]}")
+    return out
+
+
 def to_host_counts(hy):
     return hy.h_counts.numpy()
 
@@ -149,6 +192,9 @@ def main() -> int:
                     help="also time N hybrid layer calls (offloaded experts on the host, Section IV-D.2); "
                          "reported as an extra object, `value` stays the GPU path")
     ap.add_argument("--host-threads", type=int, default=16)
+    ap.add_argument("--trace", type=str, default="", metavar="LAGS",
+                    help="with --workload c5_stage_trace: also run the whole stage-structured trace with real "
+                         "slot copies, once per comma-separated prefetch lag (e.g. 0,8); extra object")
     ap.add_argument("--calib-copy-mib", type=int, default=0,
                     help="run one plain device copy of this many MiB first (counter calibration)")
     args = ap.parse_args()
@@ -304,6 +350,10 @@ def main() -> int:
     }
     if args.hybrid > 0:
         result["hybrid"] = hybrid_timings(layer, dev, args.hybrid, args.host_threads)
+    if args.trace:
+        del copies, dev
+        torch.cuda.empty_cache()
+        result["trace"] = trace_timings(args.seed, [int(v) for v in args.trace.split(",")])
     if not args.no_cpu_baseline:
         log("[bench] timing the CPU oracle")
         result["cpu_baseline"] = cpu_baseline(layer, args.cpu_seconds)

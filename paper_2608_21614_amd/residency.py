@@ -63,16 +63,23 @@ class StageResidencyRunner:
         self.out = torch.empty((T, H), dtype=self.tdtype, device=device)
         self.copy_stream = torch.cuda.Stream(device=device)
         self._pinned: Dict[tuple, tuple] = {}
+        self.reset(lag)
+
+    def reset(self, lag: int) -> None:
+        """Back to the trace's initial residency (slots refilled, logs cleared); host buffers are kept."""
+        c, L, E, dev = self.cfg, self.cfg.layers, self.cfg.experts, self.device
+        self.lag = int(lag)
         # initial residency: experts of initial_resident in ascending id take slots 0..N-1
         self.slot = np.full((L, E), -1, dtype=np.int32)
         for l in range(L):
-            ids = np.flatnonzero(trace.initial_resident[l])
+            ids = np.flatnonzero(self.trace.initial_resident[l])
             self.slot[l, ids] = np.arange(len(ids), dtype=np.int32)
-        self.d_slot = [to_device(self.slot[l], device) for l in range(L)]
+        self.d_slot = [to_device(self.slot[l], dev) for l in range(L)]
+        self.log.zero_()
         for l in range(L):
             for e in np.flatnonzero(self.slot[l] >= 0):
-                self._copy_expert(l, int(e), int(self.slot[l, e]), torch.cuda.current_stream(device))
-        torch.cuda.synchronize(device)
+                self._copy_expert(l, int(e), int(self.slot[l, e]), torch.cuda.current_stream(dev))
+        torch.cuda.synchronize(dev)
         self.copies: List[dict] = []      # one record per boundary with copies
 
     # -- weights --------------------------------------------------------------
