@@ -131,6 +131,38 @@ def hybrid_timings(layer, dev, n: int, threads: int):
     return med
 
 
+def bookkeeping_timings(dev, n: int):
+    """Median wall time per synchronised call: fused repacked forward vs the bookkeeping baseline."""
+    import numpy as np
+    import torch
+    from paper_2608_21614_amd.bookkeeping import BookkeepingLayer
+    log(f"[bench] bookkeeping A/B: {n} calls each")
+    bk = BookkeepingLayer(dev)
+    o = dev.alloc_outputs()
+    args = dev.args(o)
+    import paper_2608_21614_amd as moe
+
+    def fused():
+        moe.moe_layer_forward(args, dev.ws)
+
+    def timed(fn):
+        ts = []
+        for i in range(n + 3):
+            torch.cuda.synchronize()
+            t0 = time.perf_counter()
+            fn()
+            torch.cuda.synchronize()
+            if i >= 3:
+                ts.append((time.perf_counter() - t0) * 1e3)
+        return float(np.median(ts))
+
+    f_ms = timed(fused)
+    b_ms = timed(bk.forward)
+    return {"fused_ms": f_ms, "bookkeeping_ms": b_ms, "speedup": b_ms / f_ms,
+            "resident_experts": len(bk.resident), "host_syncs_per_call": bk.last["host_syncs"],
+            "timing": "wall clock per call, device synchronised before and after each call"}
+
+
 def trace_timings(seed: int, lags):
     """The stage-structured decode trace with real slot copies (Section IV-C), per prefetch lag.
 
@@ -192,6 +224,9 @@ def main() -> int:
                     help="also time N hybrid layer calls (offloaded experts on the host, Section IV-D.2); "
                          "reported as an extra object, `value` stays the GPU path")
     ap.add_argument("--host-threads", type=int, default=16)
+    ap.add_argument("--bookkeeping", type=int, default=0, metavar="N",
+                    help="also time N calls of the bookkeeping baseline (per-expert mask/gather/FFN/scatter) "
+                         "against N fused calls, each synchronised; extra object")
     ap.add_argument("--trace", type=str, default="", metavar="LAGS",
                     help="with --workload c5_stage_trace: also run the whole stage-structured trace with real "
                          "slot copies, once per comma-separated prefetch lag (e.g. 0,8); extra object")
@@ -348,6 +383,8 @@ def main() -> int:
         "mfma_tflops_layer_algorithmic": alg["flops"] / (ms_per_step * 1e-3) / 1e12,
         "roofline": roofline,
     }
+    if args.bookkeeping > 0:
+        result["bookkeeping"] = bookkeeping_timings(dev, args.bookkeeping)
     if args.hybrid > 0:
         result["hybrid"] = hybrid_timings(layer, dev, args.hybrid, args.host_threads)
     if args.trace:

@@ -276,6 +276,12 @@ def test_layer_c3_shared_decode(moe, seed):
     run_and_check_layer(moe, SyntheticLayer(CONFIGS["c3_shared_decode"], seed))
 
 
+@pytest.mark.parametrize("seed", [0, 1])
+def test_layer_c6_qwen3_decode(moe, seed):
+    say("layer c6_qwen3_decode seed", seed)
+    run_and_check_layer(moe, SyntheticLayer(CONFIGS["c6_qwen3_decode"], seed))
+
+
 def test_layer_c4_prefill_sampled(moe):
     say("layer c4_prefill seed 0 (sampled tokens)")
     lay = SyntheticLayer(CONFIGS["c4_prefill"], 0)

@@ -137,6 +137,12 @@ CONFIGS: Dict[str, MoEConfig] = {
         "c4_prefill", "bf16", tokens=2048, hidden=2048, experts=64, ffn=1408, top_k=6,
         shared=2, shared_ffn=1408, n_resident=48, residency="zipf_top", bias="zipf",
         description="bf16 prefill chunk of 2048 tokens, H 2048, 64 routed F 1408 top-6 + 2 shared F 1408, 48/64 resident, Zipf(1.1)"),
+    # many small experts with a wide top-k (the Qwen3-MoE family the paper evaluates): the
+    # shape of the bookkeeping A/B, where per-expert launches cost the most
+    "c6_qwen3_decode": MoEConfig(
+        "c6_qwen3_decode", "bf16", tokens=64, hidden=2048, experts=128, ffn=768, top_k=8,
+        n_resident=64, residency="zipf_top", bias="zipf",
+        description="Qwen3-MoE-like bf16 decode batch of 64 tokens, H 2048, 128 experts F 768, top-8, 64/128 resident, Zipf(1.1)"),
 }
 
 
