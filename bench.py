@@ -103,13 +103,27 @@ def cpu_baseline(layer, seconds: float):
                       f"router + repack, fp64 C with OpenMP), {el:.1f} s"}
 
 
-def hybrid_timings(layer, dev, n: int, threads: int):
+# rates of this machine (MI355X machine, 16 host threads): host->device copies, the host FFN on
+# expert weights and in FLOPs, the device FFN on expert weights -- the cost model's inputs
+LINK_GBPS, HOST_GBPS, HOST_GFLOPS, GPU_GBPS = 55.0, 90.0, 500.0, 5900.0
+
+
+def hybrid_timings(layer, dev, n: int, threads: int, spare: int = 0):
     """Median timings of n hybrid calls: GPU resident/shared experts, host offloaded experts, merge."""
     import numpy as np
     import torch
+    import paper_2608_21614_amd as moe
+    from paper_2608_21614_amd.device import DeviceLayer
     from paper_2608_21614_amd.hybrid import HybridLayer
-    log(f"[bench] hybrid: {n} calls, {threads} host threads")
-    hy = HybridLayer(dev, layer.w13, layer.w2, threads=threads)
+    log(f"[bench] hybrid: {n} calls, {threads} host threads, {spare} spare slots")
+    rates = None
+    if spare > 0:
+        c = layer.cfg
+        b = 2 if c.dtype == "bf16" else 4
+        rates = moe.moe_offload_rates(3 * c.hidden * c.ffn * b, 6 * c.hidden * c.ffn, LINK_GBPS, HOST_GBPS,
+                                      HOST_GFLOPS, GPU_GBPS)
+        dev = DeviceLayer(layer, n_slots=int(layer.resident.sum()) + spare)
+    hy = HybridLayer(dev, layer.w13, layer.w2, threads=threads, rates=rates)
     for _ in range(2):
         hy.forward()
         torch.cuda.synchronize()
@@ -118,13 +132,17 @@ def hybrid_timings(layer, dev, n: int, threads: int):
         hy.forward()
         torch.cuda.synchronize()
         rows.append(hy.timings())
-    med = {k: float(np.median([r[k] for r in rows])) for k in rows[0] if k != "host_t0"}
+    keys = set().union(*[r.keys() for r in rows]) - {"host_t0"}
+    med = {k: float(np.median([r.get(k, 0.0) for r in rows])) for k in sorted(keys)}
+    med["cost_model"] = None if rates is None else {"link_GBps": LINK_GBPS, "host_GBps": HOST_GBPS,
+                                                    "host_GFLOPs": HOST_GFLOPS, "gpu_GBps": GPU_GBPS,
+                                                    "spare_slots": spare}
     c = layer.cfg
     b = 2 if c.dtype == "bf16" else 4
-    n_off_experts = int(sum(1 for e in range(c.experts) if not layer.resident[e] and
-                            (to_host_counts(hy)[e] > 0)))
+    cnt, seg, nres = hy.h_counts.numpy(), hy.h_seg.numpy(), int(hy.h_nres[0])
+    n_off_experts = int(((cnt > 0) & (seg >= nres)).sum())      # experts the host ran in the last call
     host_bytes = n_off_experts * 3 * c.hidden * c.ffn * b
-    med["offloaded_experts"] = n_off_experts
+    med["host_experts"] = n_off_experts
     med["host_weight_bytes"] = host_bytes
     med["host_ffn_GBps"] = host_bytes / (med["host_ffn_ms"] * 1e-3) / 1e9 if med["host_ffn_ms"] > 0 else None
     med["threads"] = threads
@@ -206,10 +224,6 @@ def trace_timings(seed: int, lags):
     return out
 
 
-def to_host_counts(hy):
-    return hy.h_counts.numpy()
-
-
 def main() -> int:
     ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
     ap.add_argument("--gpus", type=int, default=1)
@@ -224,6 +238,8 @@ def main() -> int:
                     help="also time N hybrid layer calls (offloaded experts on the host, Section IV-D.2); "
                          "reported as an extra object, `value` stays the GPU path")
     ap.add_argument("--host-threads", type=int, default=16)
+    ap.add_argument("--hybrid-spare", type=int, default=0, metavar="S",
+                    help="with --hybrid: S spare device slots and the per-expert cost model (copy vs host)")
     ap.add_argument("--bookkeeping", type=int, default=0, metavar="N",
                     help="also time N calls of the bookkeeping baseline (per-expert mask/gather/FFN/scatter) "
                          "against N fused calls, each synchronised; extra object")
@@ -386,7 +402,7 @@ def main() -> int:
     if args.bookkeeping > 0:
         result["bookkeeping"] = bookkeeping_timings(dev, args.bookkeeping)
     if args.hybrid > 0:
-        result["hybrid"] = hybrid_timings(layer, dev, args.hybrid, args.host_threads)
+        result["hybrid"] = hybrid_timings(layer, dev, args.hybrid, args.host_threads, args.hybrid_spare)
     if args.trace:
         del copies, dev
         torch.cuda.empty_cache()

@@ -18,7 +18,7 @@
  * Conventions for every call
  *   - Returns moe_status.  No exception or abort crosses the ABI.
  *   - All tensor pointers are DEVICE pointers owned by the caller (except for
- *     the host-side calls moe_stage_plan and moe_host_ffn).  The library never
+ *     the host-side calls moe_stage_plan, moe_host_ffn and moe_offload_plan).  The library never
  *     allocates or frees device memory and never synchronises the stream.
  *   - Work is enqueued on `stream` (a hipStream_t; NULL is the null stream).
  *   - Arguments are validated on the host before anything is enqueued; a call
@@ -281,6 +281,34 @@ moe_status moe_stage_plan(int32_t experts, int32_t slots, const int64_t* log, co
 moe_status moe_host_ffn(const moe_dims* dims, const int32_t* counts, const int32_t* seg_start, int32_t n_res,
                         const void* const* w13, const void* const* w2, const void* off_rows, float* y_off,
                         int32_t threads, uint32_t flags);
+
+/* Measured rates of the two ways to run an offloaded expert (moe_offload_plan). */
+typedef struct moe_offload_rates {
+    double expert_bytes;    /* weight bytes of one expert (3 * H * F * dtype size for SwiGLU) */
+    double flops_per_pair;  /* FLOPs of one routed pair through one expert (6 * H * F) */
+    double link_GBps;       /* host -> device copy rate */
+    double host_GBps;       /* host FFN rate on expert weights (memory-bound regime) */
+    double host_GFLOPs;     /* host FFN rate in FLOPs (compute-bound regime) */
+    double gpu_GBps;        /* device FFN rate on expert weights */
+} moe_offload_rates;
+
+/*
+ * Per-expert choice between the two execution paths of an offloaded expert
+ * (Section IV-D.1): copy it to the GPU, or run it on the host where its weights
+ * are.  For every expert that is not resident and has routed pairs:
+ *   t_host = max(expert_bytes / host rate, counts[e] * flops_per_pair / host FLOP rate)
+ *   t_gpu  = expert_bytes / link rate + expert_bytes / device rate
+ * and an expert is a candidate for the copy when t_gpu < t_host -- few tokens
+ * favour the host, many favour the copy.  Candidates are taken largest saving
+ * first, at most max_copies, while taking one more still shortens the longer of
+ * the two queues: the host's (the t_host of the experts it keeps, run one after
+ * another on all its threads) and the link's (the t_gpu of the copied ones).
+ *   counts [E], expert_slot [E] (host copies); choice [E] (host) out:
+ *   1 = copy to the GPU, 0 = run on the host, -1 = resident or idle.
+ * Host memory only; no device work.
+ */
+moe_status moe_offload_plan(int32_t experts, const int32_t* counts, const int32_t* expert_slot, int32_t slots,
+                            const moe_offload_rates* rates, int32_t max_copies, int32_t* choice);
 
 #ifdef __cplusplus
 }

@@ -26,7 +26,7 @@ MOE_HOST_PIN = 1
 EXPORTED = [
     "moe_abi_version", "moe_status_str", "moe_check_dims", "moe_workspace_bytes", "moe_route_topk",
     "moe_repack", "moe_grouped_ffn", "moe_combine", "moe_layer_forward", "moe_stage_accumulate",
-    "moe_stage_plan", "moe_pack_weights", "moe_host_ffn",
+    "moe_stage_plan", "moe_pack_weights", "moe_host_ffn", "moe_offload_plan",
 ]
 
 
@@ -42,6 +42,11 @@ class moe_dims(ctypes.Structure):
 
 
 _vp = ctypes.c_void_p
+
+
+class moe_offload_rates(ctypes.Structure):
+    _fields_ = [(n, ctypes.c_double) for n in
+                ("expert_bytes", "flops_per_pair", "link_GBps", "host_GBps", "host_GFLOPs", "gpu_GBps")]
 
 
 class moe_layer_args(ctypes.Structure):
@@ -102,6 +107,7 @@ def _load() -> ctypes.CDLL:
         "moe_pack_weights": ([_vp, _vp, ctypes.c_int64, ctypes.c_int64, i32, _vp], ctypes.c_int),
         "moe_host_ffn": ([D, _vp, _vp, i32, ctypes.POINTER(_vp), ctypes.POINTER(_vp), _vp, _vp, i32, u32],
                          ctypes.c_int),
+        "moe_offload_plan": ([i32, _vp, _vp, i32, ctypes.POINTER(moe_offload_rates), i32, _vp], ctypes.c_int),
     }
     for name, (args, res) in sig.items():
         fn = getattr(lib, name)
@@ -243,6 +249,17 @@ def moe_host_ffn(dims, counts, seg_start, n_res: int, w13_host, w2_host, off_row
                             y_off.ctypes.data if n_off > 0 else None, int(threads),
                             MOE_HOST_PIN if pin else 0), "moe_host_ffn")
     return y_off
+
+
+def moe_offload_plan(counts, expert_slot, slots: int, rates: moe_offload_rates, max_copies: int):
+    """Per-expert choice for offloaded experts (host arrays): 1 copy to the GPU, 0 host, -1 resident/idle."""
+    import numpy as np
+    cnt = np.ascontiguousarray(counts, dtype=np.int32)
+    sl = np.ascontiguousarray(expert_slot, dtype=np.int32)
+    out = np.empty_like(cnt)
+    _check(lib.moe_offload_plan(int(cnt.size), cnt.ctypes.data, sl.ctypes.data, int(slots), ctypes.byref(rates),
+                                int(max_copies), out.ctypes.data), "moe_offload_plan")
+    return out
 
 
 def moe_stage_plan(log_host, prev_slot_host, slots: int):

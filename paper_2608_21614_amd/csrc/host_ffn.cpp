@@ -288,4 +288,47 @@ moe_status moe_host_ffn(const moe_dims* dims, const int32_t* counts, const int32
     return MOE_OK;
 }
 
+moe_status moe_offload_plan(int32_t experts, const int32_t* counts, const int32_t* expert_slot, int32_t slots,
+                            const moe_offload_rates* rates, int32_t max_copies, int32_t* choice) {
+    if (experts <= 0 || experts > 256 || !counts || !expert_slot || !rates || !choice || slots < 0 ||
+        max_copies < 0)
+        return MOE_ERR_INVALID_ARG;
+    const moe_offload_rates& r = *rates;
+    if (!(r.expert_bytes > 0) || !(r.flops_per_pair > 0) || !(r.link_GBps > 0) || !(r.host_GBps > 0) ||
+        !(r.host_GFLOPs > 0) || !(r.gpu_GBps > 0))
+        return MOE_ERR_INVALID_ARG;
+    struct Cand {
+        int e;
+        double t_host, t_gpu;
+    };
+    std::vector<Cand> cand;
+    double host_total = 0.0;
+    for (int e = 0; e < experts; ++e) {
+        const bool resident = expert_slot[e] >= 0 && expert_slot[e] < slots;
+        choice[e] = -1;
+        if (resident || counts[e] <= 0) continue;
+        choice[e] = 0;
+        // host: stream the expert's weights from host memory, or its FLOPs, whichever is slower
+        const double t_host = std::max(r.expert_bytes / (r.host_GBps * 1e9), counts[e] * r.flops_per_pair / (r.host_GFLOPs * 1e9));
+        // GPU: copy the weights over the host link, then stream them from HBM once
+        const double t_gpu = r.expert_bytes / (r.link_GBps * 1e9) + r.expert_bytes / (r.gpu_GBps * 1e9);
+        host_total += t_host;
+        if (t_gpu < t_host) cand.push_back({e, t_host, t_gpu});
+    }
+    // largest saving first; the host runs its experts one after another on all its
+    // threads and the copies queue on the link, so stop once another copy would not
+    // shorten the longer of the two queues
+    std::stable_sort(cand.begin(), cand.end(),
+                     [](const Cand& a, const Cand& b) { return a.t_host - a.t_gpu > b.t_host - b.t_gpu; });
+    double link_total = 0.0;
+    for (size_t i = 0; i < cand.size() && (int)i < max_copies; ++i) {
+        const Cand& c = cand[i];
+        if (std::max(host_total - c.t_host, link_total + c.t_gpu) >= std::max(host_total, link_total)) break;
+        host_total -= c.t_host;
+        link_total += c.t_gpu;
+        choice[c.e] = 1;
+    }
+    return MOE_OK;
+}
+
 }  // extern "C"

@@ -22,12 +22,12 @@ def say(*a):
     print("[hybrid]", *a, flush=True)
 
 
-def run_hybrid(lay, sample=None, threads=16):
+def run_hybrid(lay, sample=None, threads=16, rates=None, spare_slots=0):
     from paper_2608_21614_amd.device import DeviceLayer, to_host
     from paper_2608_21614_amd.hybrid import HybridLayer
     c = lay.cfg
-    dev = DeviceLayer(lay)
-    hy = HybridLayer(dev, lay.w13, lay.w2, threads=threads)
+    dev = DeviceLayer(lay, n_slots=int(lay.resident.sum()) + spare_slots)
+    hy = HybridLayer(dev, lay.w13, lay.w2, threads=threads, rates=rates)
     out = hy.forward()
     torch.cuda.synchronize()
     lg_ref = oracle.router_logits(lay.x, lay.w_router, lay.bias)
@@ -38,7 +38,12 @@ def run_hybrid(lay, sample=None, threads=16):
     np.testing.assert_array_equal(idx, exp_idx)
     ref = oracle.layer_forward_synthetic(lay, idx=exp_idx, sample=sample, offloaded=True)
     n_res = int(to_host(hy.o["n_res"])[0])
-    assert n_res == ref["n_res"]
+    # resident pairs under the map the call ran with (the base map, plus any experts copied in)
+    call_map = to_host(hy.d_map)
+    resident = (call_map >= 0) & (call_map < dev.slots)
+    assert n_res == int(np.bincount(exp_idx.ravel(), minlength=c.experts)[resident].sum())
+    if not hy.last.get("copied_experts"):
+        assert n_res == ref["n_res"]
     full = ref["out_res"] + ref["out_off"]
     got = host_f64(out)[ref["sample"]]
     err = rel_l2(got, full)
@@ -86,3 +91,19 @@ def test_hybrid_full_size_sampled(name, seed):
     err, n_res, _ = run_hybrid(lay, sample=sample)
     assert n_res < lay.cfg.tokens * lay.cfg.top_k
     assert err <= TOL["bf16"]
+
+
+def test_hybrid_cost_model_copies_busy_experts():
+    """With a slow host (compute-bound at 1 GFLOP/s) the cost model copies the busiest offloaded
+    experts into the two spare slots; the full layer output is unchanged."""
+    import paper_2608_21614_amd as moe
+    cfg = replace(SMALL, name="small_copy", tokens=64, top_k=4, n_resident=3)
+    H, F = cfg.hidden, cfg.ffn
+    rates = moe.moe_offload_rates(3 * H * F * 2, 6 * H * F, 50.0, 50.0, 1.0, 5000.0)
+    say("cost model: copies to spare slots")
+    err, n_res, hy = run_hybrid(SyntheticLayer(cfg, 0), rates=rates, spare_slots=2)
+    assert hy.last["copied_experts"] == 2
+    assert err <= TOL["bf16"]
+    # the two copied experts sit in the spare slots 3 and 4 of this call's map
+    from paper_2608_21614_amd.device import to_host
+    assert sorted(int(v) for v in to_host(hy.d_map) if v >= 3) == [3, 4]

@@ -138,3 +138,43 @@ def test_host_ffn_pinning_leaves_the_callers_affinity_alone():
     for _ in range(2):
         moe.moe_host_ffn(dims, rp["counts"], rp["seg_start"], n_res, w13, w2, off_rows, threads=4, pin=True)
     assert os.sched_getaffinity(0) == before
+
+
+def test_offload_plan_follows_the_latency_comparison():
+    """Section IV-D.1: copy an offloaded expert when link + device time beats the host time."""
+    H, F = 4096, 14336
+    eb, fl = 3 * H * F * 2, 6 * H * F
+    rates = moe.moe_offload_rates(eb, fl, 55.0, 90.0, 528.0, 5900.0)
+    t_gpu = eb / 55e9 + eb / 5900e9
+    # host time: max(bytes / 90 GB/s, c * flops / 528 GFLOP/s); crossover between 9 and 10 pairs
+    assert max(eb / 90e9, 9 * fl / 528e9) < t_gpu < max(eb / 90e9, 10 * fl / 528e9)
+    counts = np.array([8, 0, 3, 40, 12, 9, 10, 2], np.int32)
+    slot = np.array([0, 1, -1, -1, -1, -1, -1, -1], np.int32)
+    c = moe.moe_offload_plan(counts, slot, 2, rates, 8)
+    assert c.tolist() == [-1, -1, 0, 1, 1, 0, 1, 0]
+    # at most two copies: the largest savings (40 pairs, then 12)
+    c = moe.moe_offload_plan(counts, slot, 2, rates, 2)
+    assert c.tolist() == [-1, -1, 0, 1, 1, 0, 0, 0]
+    assert moe.moe_offload_plan(counts, slot, 2, rates, 0).tolist() == [-1, -1, 0, 0, 0, 0, 0, 0]
+    # a slot at or past `slots` is offloaded, not resident
+    c = moe.moe_offload_plan(counts, np.array([0, 5, -1, -1, -1, -1, -1, -1], np.int32), 2, rates, 8)
+    assert c[1] == -1 and c[0] == -1  # expert 1 has no pairs
+    bad = moe.moe_offload_rates(eb, fl, 0.0, 90.0, 528.0, 5900.0)
+    with pytest.raises(moe.MoeError):
+        moe.moe_offload_plan(counts, slot, 2, bad, 8)
+
+
+def test_offload_plan_balances_host_and_link():
+    """Six busy experts: copying stops once the link queue would outgrow the host queue."""
+    H, F = 4096, 14336
+    eb, fl = 3 * H * F * 2, 6 * H * F
+    rates = moe.moe_offload_rates(eb, fl, 55.0, 90.0, 528.0, 5900.0)
+    t_host, t_gpu = 20 * fl / 528e9, eb / 55e9 + eb / 5900e9
+    counts = np.array([0, 0] + [20] * 6, np.int32)
+    slot = np.array([0, 1, -1, -1, -1, -1, -1, -1], np.int32)
+    m = 0   # copies the greedy balance takes, computed from the queue lengths
+    while m < 6 and max((6 - m - 1) * t_host, (m + 1) * t_gpu) < max((6 - m) * t_host, m * t_gpu):
+        m += 1
+    assert m == 4
+    c = moe.moe_offload_plan(counts, slot, 2, rates, 8)
+    assert c.tolist() == [-1, -1, 1, 1, 1, 1, 0, 0]     # equal savings: lower ids first
