@@ -252,20 +252,11 @@ moe_status moe_layer_forward(const moe_layer_args* a, void* ws, size_t ws_bytes,
     };
 
     hipError_t e = mark(hipSuccess, 0);
-    if (saem::front_small_fits(s)) {
-        // one workgroup routes and repacks a decode batch; both stage events mark its end
-        if (e == hipSuccess)
-            e = mark(saem::launch_front_small(s, a->x, a->w_router, lin ? nullptr : a->bias, logits, lin, idx, w,
-                                              at<float>(ws, L.part), a->expert_slot, counts, seg, perm, inv, nres, hs),
-                     1);
-        if (e == hipSuccess) e = mark(hipSuccess, 2);
-    } else {
-        if (e == hipSuccess)
-            e = mark(saem::launch_route_topk(s, a->x, a->w_router, lin ? nullptr : a->bias, logits, lin, idx, w,
-                                             nullptr, hs),
-                     1);
-        if (e == hipSuccess) e = mark(saem::launch_repack(s, idx, a->expert_slot, counts, seg, perm, inv, nres, hs), 2);
-    }
+    if (e == hipSuccess)
+        e = mark(saem::launch_route_topk(s, a->x, a->w_router, lin ? nullptr : a->bias, logits, lin, idx, w,
+                                         at<float>(ws, L.part), hs),
+                 1);
+    if (e == hipSuccess) e = mark(saem::launch_repack(s, idx, a->expert_slot, counts, seg, perm, inv, nres, hs), 2);
     if (s.T == 0) {
         for (int i = 3; i < MOE_STAGE_EVENTS && e == hipSuccess; ++i) e = mark(hipSuccess, i);
         return hip_status(e);

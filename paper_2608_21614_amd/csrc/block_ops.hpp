@@ -1,5 +1,5 @@
 // block_ops.hpp -- workgroup-level building blocks of the routing front end:
-// router scores on MFMA, the rank-based top-k gate, and the single-workgroup
+// router scores on MFMA, the wave-argmax top-k gate, and the single-workgroup
 // counting sort that repacks the (token, expert) pairs.
 #pragma once
 
@@ -35,22 +35,32 @@ __device__ __forceinline__ int wave_max_i32(int v) {
     return max(max(r0, r1), max(r2, r3));
 }
 
+__device__ __forceinline__ int wave_min_i32(int v) {
+    v = min(v, __builtin_amdgcn_mov_dpp(v, 0xB1, 0xF, 0xF, true));
+    v = min(v, __builtin_amdgcn_mov_dpp(v, 0x4E, 0xF, 0xF, true));
+    v = min(v, __builtin_amdgcn_mov_dpp(v, 0x124, 0xF, 0xF, true));
+    v = min(v, __builtin_amdgcn_mov_dpp(v, 0x128, 0xF, 0xF, true));
+    const int r0 = __builtin_amdgcn_readlane(v, 0), r1 = __builtin_amdgcn_readlane(v, 16);
+    const int r2 = __builtin_amdgcn_readlane(v, 32), r3 = __builtin_amdgcn_readlane(v, 48);
+    return min(min(r0, r1), min(r2, r3));
+}
+
 // LDS the top-k needs: selected (score, expert) of up to 64 rows x 8.
 constexpr int kTopkLdsWords = 2 * 64 * 8;
 
 // Top-k gate of `rows` tokens whose scores sit in LDS (s_lg, pitch kLgPitch),
 // by the whole workgroup.  Experts are totally ordered by (score desc, expert
 // id asc); the rank of expert e in row t is the number of experts before it in
-// that order, and e is the j-th choice of t iff its rank is j < k.  For E <= 64
-// one wave per token with one expert per lane picks the choices in rank order
-// (k rounds of a wave argmax); for larger E every (t, e) counts its rank in
-// parallel.  The gate of choice j is exp(s_j - s_0) /
+// that order, and e is the j-th choice of t iff its rank is j < k.  One wave
+// per token picks the choices in rank order, k rounds of a wave argmax over
+// integer keys with the scores' order: one expert per lane for E <= 64, up to
+// four per lane (E <= 256) with the lowest id among the lanes' equal offers.  The gate of choice j is exp(s_j - s_0) /
 // sum_j' exp(s_j' - s_0), summed in j order; a score equal to the top one
 // contributes exactly 1 (so all-equal rows, -inf included, get 1/k).
 // Writes out_idx/out_w rows [t0, t0 + rows) and, if given, lds_idx[t*k + j].
 // Ends with a barrier.  (NaN scores: undefined selection, never an index
 // outside [-1, E).)
-__device__ inline void topk_rank_block(const float* s_lg, int rows, int E, int k, int t0, int32_t* out_idx,
+__device__ inline void topk_block(const float* s_lg, int rows, int E, int k, int t0, int32_t* out_idx,
                                        float* out_w, int32_t* lds_idx, float* s_selv, int* s_sele) {
     for (int i = threadIdx.x; i < rows * 8; i += blockDim.x) s_sele[i] = -1;
     __syncthreads();
@@ -75,18 +85,36 @@ __device__ inline void topk_rank_block(const float* s_lg, int rows, int E, int k
             }
         }
     } else {
-        for (int idx = threadIdx.x; idx < rows * E; idx += blockDim.x) {
-            const int t = idx / E, e = idx % E;
-            const float* row = s_lg + t * kLgPitch;
-            const float v = row[e];
-            int rank = 0;
-            for (int e2 = 0; e2 < E; ++e2) {
-                const float v2 = row[e2];
-                rank += (v2 > v || (v2 == v && e2 < e)) ? 1 : 0;
+        // E <= 256: lane l holds experts l, l + 64, l + 128, l + 192.  Each round a
+        // lane offers its best open expert (largest key, then lowest id), the wave
+        // takes the largest key, and among the lanes offering it the lowest id.
+        const int lane = lane_id(), nw = blockDim.x / kWave;
+        for (int t = threadIdx.x / kWave; t < rows; t += nw) {
+            int key[4];
+            bool open[4];
+#pragma unroll
+            for (int sl = 0; sl < 4; ++sl) {
+                const int e = lane + kWave * sl;
+                open[sl] = e < E;
+                key[sl] = score_key(open[sl] ? s_lg[t * kLgPitch + e] : 0.f);
             }
-            if (rank < k) {
-                s_selv[t * 8 + rank] = v;
-                s_sele[t * 8 + rank] = e;
+            for (int j = 0; j < k; ++j) {
+                int kb = INT_MIN, eb = INT_MAX;
+#pragma unroll
+                for (int sl = 0; sl < 4; ++sl)
+                    if (open[sl] && (eb == INT_MAX || key[sl] > kb)) {
+                        kb = key[sl];
+                        eb = lane + kWave * sl;
+                    }
+                const int m = wave_max_i32(eb != INT_MAX ? kb : INT_MIN);
+                const int e = wave_min_i32((eb != INT_MAX && kb == m) ? eb : INT_MAX);  // never INT_MAX: k <= E
+#pragma unroll
+                for (int sl = 0; sl < 4; ++sl)
+                    if (lane + kWave * sl == e) open[sl] = false;
+                if (lane == 0 && e != INT_MAX) {
+                    s_selv[t * 8 + j] = s_lg[t * kLgPitch + e];
+                    s_sele[t * 8 + j] = e;
+                }
             }
         }
     }

@@ -22,13 +22,8 @@ int router_slices(const Shape& s);
 hipError_t launch_route_topk(const Shape& s, const void* x, const void* w_router, const float* bias, float* logits,
                              bool logits_in, int32_t* topk_idx, float* topk_w, float* part, hipStream_t st);
 
-// Decode front end (T <= 64): scores + top-k + repacking, two launches.
-hipError_t launch_front_small(const Shape& s, const void* x, const void* w_router, const float* bias, float* logits,
-                              bool logits_in, int32_t* topk_idx, float* topk_w, float* part,
-                              const int32_t* expert_slot, int32_t* counts, int32_t* seg_start, int32_t* perm,
-                              int32_t* inv_perm, int32_t* n_res, hipStream_t st);
-
-// Histogram, group-order scan, stable permutation, residency split.
+// Expert-aligned repacking: histogram, group-order scan, stable permutation,
+// residency split (one workgroup).
 hipError_t launch_repack(const Shape& s, const int32_t* topk_idx, const int32_t* expert_slot, int32_t* counts,
                          int32_t* seg_start, int32_t* perm, int32_t* inv_perm, int32_t* n_res, hipStream_t st);
 

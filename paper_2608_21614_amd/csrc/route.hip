@@ -6,13 +6,13 @@
 //
 //  * T > 64 (prefill): k_route_topk, 16 tokens per 1024-thread workgroup whose
 //    16 waves split K and add their partial tiles in a fixed order.
-// The top-k ranks every (token, expert) in parallel (topk_rank_block).
+// The top-k takes one wave per token (topk_block: k rounds of a wave argmax).
 //  * T <= 64 (decode): k_router_partial spreads the scores over one workgroup
 //    per K slice (a single CU cannot stream the batch and the router fast
-//    enough), then k_front_small adds the slices in order and runs the top-k
-//    and, in the fused forward, the expert-aligned repacking of all pairs in one
-//    workgroup.  moe_route_topk uses the same two kernels, so both paths give
-//    bit-identical scores.
+//    enough), then k_route_finish adds each token's slices in order and runs its
+//    top-k, one wave per token over many CUs.  The fused forward and
+//    moe_route_topk use the same two kernels, so both give bit-identical scores;
+//    the repacking follows in k_repack.
 #include "block_ops.hpp"
 #include "kernels.hpp"
 
@@ -45,7 +45,7 @@ __global__ void __launch_bounds__(kFrontThreads)
         else logits[(size_t)(t0 + row) * E + e] = s_lg[row * kLgPitch + e];
     }
     __syncthreads();
-    topk_rank_block(s_lg, rows, E, k, t0, topk_idx, topk_w, nullptr, s_selv, s_sele);
+    topk_block(s_lg, rows, E, k, t0, topk_idx, topk_w, nullptr, s_selv, s_sele);
 }
 
 // Decode batches: part[slice][t][e] = sum over the slice's K steps of x[t] . w_router[e].
@@ -100,66 +100,93 @@ __global__ void __launch_bounds__(256)
     }
 }
 
-// Decode front end in one workgroup: adds the K-sliced partial scores in slice
-// order (+ bias), runs the top-k and, if `repack`, repacks all pairs.
-__global__ void __launch_bounds__(kFrontThreads)
-    k_front_small(int T, int E, int k, int slots, const float* __restrict__ part, int nsl,
-                  const float* __restrict__ bias, float* __restrict__ logits, int logits_in,
-                  int32_t* __restrict__ topk_idx, float* __restrict__ topk_w, int repack,
-                  const int32_t* __restrict__ expert_slot, int32_t* __restrict__ counts,
-                  int32_t* __restrict__ seg_start, int32_t* __restrict__ perm, int32_t* __restrict__ inv_perm,
-                  int32_t* __restrict__ n_res) {
-    __shared__ float s_lg[64 * kLgPitch];
-    __shared__ int s_rep[kRepackLdsInts];
-    __shared__ int32_t s_idx[64 * 8];
-    __shared__ float s_selv[64 * 8];
-    __shared__ int s_sele[64 * 8];
-    if (!logits_in) {
-        // add the K-sliced partials in slice order (+ bias); 4 entries x 16 slices of loads in flight per thread
-        constexpr int kPer = 4;
-        for (int base = threadIdx.x; base < T * E; base += kPer * kFrontThreads) {
-            float v[kPer];
+// Decode front end, second step: one wave per token adds the token's K-sliced
+// partial scores in slice order (+ bias) and writes them to logits (or reads the
+// caller's scores), then picks the token's top-k in rank order with k rounds of
+// a wave argmax over integer keys with the scores' order: lane l holds experts
+// l, l + 64, l + 128, l + 192, offers its best open one (largest key, then lowest
+// id), and the wave takes the largest key and, among the lanes offering it, the
+// lowest id.  The gate of choice j is exp(s_j - s_0) / sum_j' exp(s_j' - s_0),
+// summed in j order; a score equal to the top one contributes exactly 1.
+__global__ void __launch_bounds__(256)
+    k_route_finish(int T, int E, int k, const float* __restrict__ part, int nsl, const float* __restrict__ bias,
+                   float* __restrict__ logits, int logits_in, int32_t* __restrict__ topk_idx,
+                   float* __restrict__ topk_w) {
+    const int lane = lane_id();
+    const int t = blockIdx.x * 4 + (threadIdx.x >> 6);
+    if (t >= T) return;  // the whole wave
+    float v[4];
+    int key[4];
+    bool open[4];
 #pragma unroll
-            for (int i = 0; i < kPer; ++i) v[i] = 0.f;
+    for (int sl = 0; sl < 4; ++sl) {
+        const int e = lane + kWave * sl;
+        open[sl] = e < E;
+        v[sl] = 0.f;
+        if (kWave * sl >= E) continue;  // uniform
+        if (logits_in) {
+            if (open[sl]) v[sl] = logits[(size_t)t * E + e];
+        } else {
+            const float* p = part + (size_t)t * E + (open[sl] ? e : 0);
+            float acc = 0.f;
             for (int b = 0; b < nsl; b += 16) {
-                float p[kPer][16];
+                float q[16];
 #pragma unroll
-                for (int i = 0; i < kPer; ++i) {
-                    const int idx = base + i * kFrontThreads;
+                for (int j = 0; j < 16; ++j) q[j] = (b + j < nsl) ? p[(size_t)(b + j) * 64 * E] : 0.f;
 #pragma unroll
-                    for (int j = 0; j < 16; ++j)
-                        p[i][j] = (idx < T * E && b + j < nsl) ? part[(size_t)(b + j) * 64 * E + idx] : 0.f;
-                }
-#pragma unroll
-                for (int i = 0; i < kPer; ++i)
-#pragma unroll
-                    for (int j = 0; j < 16; ++j)
-                        if (b + j < nsl) v[i] = (b + j == 0) ? p[i][j] : v[i] + p[i][j];
+                for (int j = 0; j < 16; ++j)
+                    if (b + j < nsl) acc = (b + j == 0) ? q[j] : acc + q[j];
             }
-#pragma unroll
-            for (int i = 0; i < kPer; ++i) {
-                const int idx = base + i * kFrontThreads;
-                if (idx < T * E) {
-                    const int t = idx / E, e = idx % E;
-                    const float sc = v[i] + (bias ? bias[e] : 0.f);
-                    s_lg[t * kLgPitch + e] = sc;
-                    logits[idx] = sc;
-                }
+            if (open[sl]) {
+                v[sl] = acc + (bias ? bias[e] : 0.f);
+                logits[(size_t)t * E + e] = v[sl];
             }
         }
-    } else {
-        for (int idx = threadIdx.x; idx < T * E; idx += kFrontThreads) s_lg[(idx / E) * kLgPitch + idx % E] = logits[idx];
     }
-    __syncthreads();
-    topk_rank_block(s_lg, T, E, k, 0, topk_idx, topk_w, s_idx, s_selv, s_sele);
-    if (!repack) return;
-    repack_block(T, E, k, slots, s_idx, expert_slot, counts, seg_start, perm, inv_perm, n_res, s_rep);
+#pragma unroll
+    for (int sl = 0; sl < 4; ++sl) key[sl] = score_key(v[sl]);
+    float selv[8];
+    int sele[8];
+#pragma unroll
+    for (int j = 0; j < 8; ++j) {
+        selv[j] = 0.f;
+        sele[j] = -1;
+        if (j >= k) continue;  // uniform
+        int kb = INT_MIN, eb = INT_MAX;
+#pragma unroll
+        for (int sl = 0; sl < 4; ++sl)
+            if (open[sl] && (eb == INT_MAX || key[sl] > kb)) {
+                kb = key[sl];
+                eb = lane + kWave * sl;
+            }
+        const int m = wave_max_i32(eb != INT_MAX ? kb : INT_MIN);
+        const int e = wave_min_i32((eb != INT_MAX && kb == m) ? eb : INT_MAX);  // never INT_MAX: k <= E
+#pragma unroll
+        for (int sl = 0; sl < 4; ++sl)
+            if (lane + kWave * sl == e) open[sl] = false;
+        const int es = e >> 6, el = e & 63;
+        float ve = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v[0]), el));
+        if (es == 1) ve = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v[1]), el));
+        if (es == 2) ve = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v[2]), el));
+        if (es == 3) ve = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v[3]), el));
+        selv[j] = ve;
+        sele[j] = e;
+    }
+    float sum = 0.f;
+#pragma unroll
+    for (int j = 0; j < 8; ++j)
+        if (j < k) sum += (selv[j] == selv[0]) ? 1.0f : expf(selv[j] - selv[0]);
+#pragma unroll
+    for (int j = 0; j < 8; ++j)
+        if (j < k && lane == j) {
+            const float term = (selv[j] == selv[0]) ? 1.0f : expf(selv[j] - selv[0]);
+            topk_idx[(size_t)t * k + j] = sele[j];
+            topk_w[(size_t)t * k + j] = term / sum;
+        }
 }
 
 hipError_t launch_small(const Shape& s, const void* x, const void* w_router, const float* bias, float* logits,
-                        bool logits_in, int32_t* topk_idx, float* topk_w, float* part, bool repack,
-                        const int32_t* expert_slot, int32_t* counts, int32_t* seg_start, int32_t* perm,
-                        int32_t* inv_perm, int32_t* n_res, hipStream_t st) {
+                        bool logits_in, int32_t* topk_idx, float* topk_w, float* part, hipStream_t st) {
     const int nsl = router_slices(s);
     if (!logits_in && s.T > 0) {
         if (s.bf16)
@@ -169,9 +196,8 @@ hipError_t launch_small(const Shape& s, const void* x, const void* w_router, con
             hipLaunchKernelGGL(k_router_partial<float>, dim3(nsl), dim3(256), 0, st, s.T, s.H, s.E, x, w_router, nsl,
                                part);
     }
-    hipLaunchKernelGGL(k_front_small, dim3(1), dim3(kFrontThreads), 0, st, s.T, s.E, s.k, s.slots, part, nsl, bias,
-                       logits, logits_in ? 1 : 0, topk_idx, topk_w, repack ? 1 : 0, expert_slot, counts, seg_start,
-                       perm, inv_perm, n_res);
+    hipLaunchKernelGGL(k_route_finish, dim3((s.T + 3) / 4), dim3(256), 0, st, s.T, s.E, s.k, part, nsl, bias, logits,
+                       logits_in ? 1 : 0, topk_idx, topk_w);
     return hipGetLastError();
 }
 
@@ -188,9 +214,7 @@ int router_slices(const Shape& s) {
 hipError_t launch_route_topk(const Shape& s, const void* x, const void* w_router, const float* bias, float* logits,
                              bool logits_in, int32_t* topk_idx, float* topk_w, float* part, hipStream_t st) {
     if (s.T == 0) return hipSuccess;
-    if (front_small_fits(s))  // same kernels and order as the decode front end
-        return launch_small(s, x, w_router, bias, logits, logits_in, topk_idx, topk_w, part, false, nullptr, nullptr,
-                            nullptr, nullptr, nullptr, nullptr, st);
+    if (front_small_fits(s)) return launch_small(s, x, w_router, bias, logits, logits_in, topk_idx, topk_w, part, st);
     const int li = logits_in ? 1 : 0;
     dim3 grid((s.T + 15) / 16), block(kFrontThreads);
     if (s.bf16)
@@ -200,14 +224,6 @@ hipError_t launch_route_topk(const Shape& s, const void* x, const void* w_router
         hipLaunchKernelGGL(k_route_topk<false>, grid, block, 0, st, s.T, s.H, s.E, s.k, x, w_router, bias, logits,
                            li, topk_idx, topk_w);
     return hipGetLastError();
-}
-
-hipError_t launch_front_small(const Shape& s, const void* x, const void* w_router, const float* bias, float* logits,
-                              bool logits_in, int32_t* topk_idx, float* topk_w, float* part,
-                              const int32_t* expert_slot, int32_t* counts, int32_t* seg_start, int32_t* perm,
-                              int32_t* inv_perm, int32_t* n_res, hipStream_t st) {
-    return launch_small(s, x, w_router, bias, logits, logits_in, topk_idx, topk_w, part, true, expert_slot, counts,
-                        seg_start, perm, inv_perm, n_res, st);
 }
 
 }  // namespace saem
