@@ -49,8 +49,8 @@ __global__ void __launch_bounds__(kFrontThreads)
 }
 
 // Decode batches: part[slice][t][e] = sum over the slice's K steps of x[t] . w_router[e].
-// One workgroup per K slice; wave w covers tokens 16w .. 16w+15; MFMA on bf16
-// (16x16x32) or fp32 (16x16x4) operands.
+// One workgroup per (K slice, chunk of 64 experts); wave w covers tokens
+// 16w .. 16w+15; MFMA on bf16 (16x16x32) or fp32 (16x16x4) operands.
 template <typename Elt>
 __global__ void __launch_bounds__(256)
     k_router_partial(int T, int H, int E, const void* __restrict__ x, const void* __restrict__ wr, int nsl,
@@ -63,7 +63,8 @@ __global__ void __launch_bounds__(256)
     if (16 * wave >= T) return;
     const int tok = 16 * wave + r;
     const Elt* xp = (tok < T) ? static_cast<const Elt*>(x) + (size_t)tok * H + kq : nullptr;
-    for (int c0 = 0; c0 < E; c0 += kScoreChunk) {
+    {
+        const int c0 = blockIdx.y * kScoreChunk;
         f32x4 acc[4];
         const Elt* wp[4];
 #pragma unroll
@@ -118,30 +119,41 @@ __global__ void __launch_bounds__(256)
     float v[4];
     int key[4];
     bool open[4];
+    const int nslot = (E + kWave - 1) / kWave;
 #pragma unroll
     for (int sl = 0; sl < 4; ++sl) {
-        const int e = lane + kWave * sl;
-        open[sl] = e < E;
+        open[sl] = lane + kWave * sl < E;
         v[sl] = 0.f;
-        if (kWave * sl >= E) continue;  // uniform
-        if (logits_in) {
-            if (open[sl]) v[sl] = logits[(size_t)t * E + e];
-        } else {
-            const float* p = part + (size_t)t * E + (open[sl] ? e : 0);
-            float acc = 0.f;
-            for (int b = 0; b < nsl; b += 16) {
-                float q[16];
+    }
+    if (logits_in) {
 #pragma unroll
-                for (int j = 0; j < 16; ++j) q[j] = (b + j < nsl) ? p[(size_t)(b + j) * 64 * E] : 0.f;
+        for (int sl = 0; sl < 4; ++sl)
+            if (open[sl]) v[sl] = logits[(size_t)t * E + lane + kWave * sl];
+    } else {
+        // all slots' loads of a batch of 16 slices in flight together, bias included
+        float bv[4];
+#pragma unroll
+        for (int sl = 0; sl < 4; ++sl) bv[sl] = (open[sl] && bias) ? bias[lane + kWave * sl] : 0.f;
+        for (int b = 0; b < nsl; b += 16) {
+            float q[4][16];
+#pragma unroll
+            for (int sl = 0; sl < 4; ++sl) {
+                const float* p = part + (size_t)t * E + (open[sl] ? lane + kWave * sl : 0);
+#pragma unroll
+                for (int j = 0; j < 16; ++j) q[sl][j] = (sl < nslot && b + j < nsl) ? p[(size_t)(b + j) * 64 * E] : 0.f;
+            }
+#pragma unroll
+            for (int sl = 0; sl < 4; ++sl)
 #pragma unroll
                 for (int j = 0; j < 16; ++j)
-                    if (b + j < nsl) acc = (b + j == 0) ? q[j] : acc + q[j];
-            }
-            if (open[sl]) {
-                v[sl] = acc + (bias ? bias[e] : 0.f);
-                logits[(size_t)t * E + e] = v[sl];
-            }
+                    if (b + j < nsl) v[sl] = (b + j == 0) ? q[sl][j] : v[sl] + q[sl][j];
         }
+#pragma unroll
+        for (int sl = 0; sl < 4; ++sl)
+            if (open[sl]) {
+                v[sl] += bv[sl];
+                logits[(size_t)t * E + lane + kWave * sl] = v[sl];
+            }
     }
 #pragma unroll
     for (int sl = 0; sl < 4; ++sl) key[sl] = score_key(v[sl]);
@@ -190,11 +202,11 @@ hipError_t launch_small(const Shape& s, const void* x, const void* w_router, con
     const int nsl = router_slices(s);
     if (!logits_in && s.T > 0) {
         if (s.bf16)
-            hipLaunchKernelGGL(k_router_partial<uint16_t>, dim3(nsl), dim3(256), 0, st, s.T, s.H, s.E, x, w_router,
-                               nsl, part);
+            hipLaunchKernelGGL(k_router_partial<uint16_t>, dim3(nsl, (s.E + kScoreChunk - 1) / kScoreChunk), dim3(256),
+                               0, st, s.T, s.H, s.E, x, w_router, nsl, part);
         else
-            hipLaunchKernelGGL(k_router_partial<float>, dim3(nsl), dim3(256), 0, st, s.T, s.H, s.E, x, w_router, nsl,
-                               part);
+            hipLaunchKernelGGL(k_router_partial<float>, dim3(nsl, (s.E + kScoreChunk - 1) / kScoreChunk), dim3(256), 0,
+                               st, s.T, s.H, s.E, x, w_router, nsl, part);
     }
     hipLaunchKernelGGL(k_route_finish, dim3((s.T + 3) / 4), dim3(256), 0, st, s.T, s.E, s.k, part, nsl, bias, logits,
                        logits_in ? 1 : 0, topk_idx, topk_w);
