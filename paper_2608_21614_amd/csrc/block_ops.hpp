@@ -1,6 +1,6 @@
 // block_ops.hpp -- workgroup-level building blocks of the routing front end:
-// router scores on MFMA, the wave-argmax top-k gate, and the single-workgroup
-// counting sort that repacks the (token, expert) pairs.
+// router scores on MFMA, the wave-argmax top-k gate, and the chunked counting
+// sort that repacks the (token, expert) pairs.
 #pragma once
 
 #include <limits.h>
@@ -216,40 +216,52 @@ __device__ inline void router_scores_f32(int T, int H, int E, const float* __res
 }
 
 // LDS ints the repack needs.
-constexpr int kRepackLdsInts = 3 * 256 + kFrontWaves * 256 + 4;
+constexpr int kRepackLdsInts = 4 * 256 + kFrontWaves * 256 + 4;
 
-// Expert-aligned repacking of T*k pairs by one 1024-thread workgroup.
-//   1. histogram with LDS atomics (order-free);
+// Expert-aligned repacking of the T*k pairs in chunks of kFrontThreads pairs
+// (chunk c = pairs [c kFrontThreads, (c + 1) kFrontThreads)); a workgroup
+// scatters the chunks [c_begin, c_end) in order:
+//   1. it counts all pairs per expert, and separately the pairs before c_begin,
+//      with LDS atomics (order-free; the ids are a few tens of KB and stay in L2);
 //   2. one wave scans the counts in group order -- resident experts by id, then
-//      offloaded experts by id -- into segment starts and n_res;
-//   3. pairs are scattered in chunks of 1024, one per thread: inside a wave the
-//      lanes holding the same expert are found with 8 ballots over the bits of
-//      the expert id, a lane's rank is the popcount of the matching lanes below
-//      it, and each wave adds the counts of the waves before it (LDS).  Pairs
-//      keep their index order inside an expert: a stable counting sort, no
-//      global atomics.
-// idx may point to global or LDS memory; ids outside [0, E) are dropped
-// (inv_perm = -1).  Ends with a barrier.
-__device__ inline void repack_block(int T, int E, int k, int slots, const int32_t* idx,
-                                    const int32_t* __restrict__ expert_slot, int32_t* __restrict__ counts,
-                                    int32_t* __restrict__ seg_start, int32_t* __restrict__ perm,
-                                    int32_t* __restrict__ inv_perm, int32_t* __restrict__ n_res, int* lds) {
+//      offloaded experts by id -- into segment starts and n_res; the first
+//      chunk's pairs of expert e start after the earlier chunks' pairs of e;
+//   3. one pair per thread per chunk: inside a wave the lanes holding the same
+//      expert are found with 8 ballots over the bits of the expert id, a lane's
+//      rank is the popcount of the matching lanes below it, and each wave adds
+//      the counts of the waves before it (LDS); after the chunk every expert's
+//      start moves past the chunk's pairs.  Pairs keep their index order inside
+//      an expert: a stable counting sort with no global atomics, and the same
+//      result for any split of the chunks over workgroups.
+// The workgroup with c_begin == 0 also writes counts, seg_start and n_res.
+// ids outside [0, E) are dropped (inv_perm = -1).
+__device__ inline void repack_chunks(int T, int E, int k, int slots, int c_begin, int c_end,
+                                     const int32_t* __restrict__ idx, const int32_t* __restrict__ expert_slot,
+                                     int32_t* __restrict__ counts, int32_t* __restrict__ seg_start,
+                                     int32_t* __restrict__ perm, int32_t* __restrict__ inv_perm,
+                                     int32_t* __restrict__ n_res, int* lds) {
     int* s_cnt = lds;
-    int* s_base = lds + 256;
-    int* s_res = lds + 512;
-    int* s_wcnt = lds + 768;                // [16][256]
-    int* s_nres = lds + 768 + kFrontWaves * 256;
+    int* s_pre = lds + 256;
+    int* s_base = lds + 512;
+    int* s_res = lds + 768;
+    int* s_wcnt = lds + 1024;               // [16][256]
+    int* s_nres = lds + 1024 + kFrontWaves * 256;
     const int tid = threadIdx.x, wave = tid >> 6, lane = lane_id();
     const int P = T * k;
+    const int c0 = c_begin * kFrontThreads;
 
     for (int e = tid; e < 256; e += kFrontThreads) {
         s_cnt[e] = 0;
+        s_pre[e] = 0;
         s_res[e] = (e < E) ? (is_resident(expert_slot[e], slots) ? 1 : 0) : 0;
     }
     __syncthreads();
     for (int q = tid; q < P; q += kFrontThreads) {
         const int e = idx[q];
-        if (e >= 0 && e < E) atomicAdd(&s_cnt[e], 1);
+        if (e >= 0 && e < E) {
+            atomicAdd(&s_cnt[e], 1);
+            if (q < c0) atomicAdd(&s_pre[e], 1);
+        }
     }
     __syncthreads();
     if (wave == 0) {
@@ -290,17 +302,20 @@ __device__ inline void repack_block(int T, int E, int k, int slots, const int32_
         if (lane == 0) *s_nres = rtot;
     }
     __syncthreads();
-    for (int e = tid; e < E; e += kFrontThreads) {
-        counts[e] = s_cnt[e];
-        seg_start[e] = s_base[e];
+    if (c_begin == 0) {
+        for (int e = tid; e < E; e += kFrontThreads) {
+            counts[e] = s_cnt[e];
+            seg_start[e] = s_base[e];
+        }
+        if (tid == 0) *n_res = *s_nres;
     }
-    if (tid == 0) *n_res = *s_nres;
+    for (int e = tid; e < E; e += kFrontThreads) s_base[e] += s_pre[e];
 
     const unsigned long long lt_mask = (1ull << lane) - 1ull;
-    for (int c0 = 0; c0 < P; c0 += kFrontThreads) {
+    for (int c = c_begin; c < c_end; ++c) {
         for (int i = tid; i < kFrontWaves * 256; i += kFrontThreads) s_wcnt[i] = 0;
         __syncthreads();
-        const int q = c0 + tid;
+        const int q = c * kFrontThreads + tid;
         const int e = (q < P) ? idx[q] : -1;
         const bool valid = (e >= 0 && e < E);
         unsigned long long m = __ballot(valid);

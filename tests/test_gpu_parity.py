@@ -147,7 +147,10 @@ def test_route_topk_computed_scores(moe, dtype, T, H, E, k, bias):
 
 @pytest.mark.parametrize("T,E,k,mode", [(1, 1, 1, "all"), (4, 4, 2, "paper"), (32, 8, 2, "random"),
                                          (64, 60, 4, "random"), (2048, 64, 6, "random"), (3000, 256, 8, "random"),
-                                         (500, 16, 3, "none"), (257, 64, 6, "all"), (40, 8, 2, "invalid")])
+                                         (500, 16, 3, "none"), (257, 64, 6, "all"), (40, 8, 2, "invalid"),
+                                         # 128 chunks of 1024 pairs (one per workgroup), then 157 (two per
+                                         # workgroup for some)
+                                         (16384, 128, 8, "all"), (20000, 64, 8, "random")])
 def test_repack_bit_exact(moe, T, E, k, mode):
     say("repack", T, E, k, mode)
     rng = np.random.default_rng(T + E * 7 + k)
