@@ -662,14 +662,24 @@ bool ffn_packs_offloaded(const Shape& s) { return use_stream(s); }
 
 int ffn_down_splits(const Shape& s) {
     if (!use_stream(s)) return 1;
-    // phase-2 work items: (groups) x (H / 64 row tiles) x ks; aim for >= ~2048
-    // workgroups while every wave keeps >= 2 K steps of 32.
-    const int groups = max_routed_groups(s) + s.S;
+    // Phase-2 work items: (groups) x (H / 64 row tiles) x ks, each streaming 64
+    // rows of one K chunk.  Smallest ks (a power of two <= 16) such that
+    //  * there are >= 512 workgroups (two per CU), and
+    //  * the longest workgroup streams at most 1/400 of the phase's weights: one
+    //    workgroup streams at about 1/200 of the chip's HBM rate, so with a 2x
+    //    margin it then ends before the phase does, instead of forming its tail
+    //    (a shared expert wider than the routed ones, or few wide experts);
+    // while every wave keeps >= 8 K steps of 32.
+    const long long groups_r = max_routed_groups(s);
+    const long long groups = groups_r + s.S;
     if (groups == 0) return 1;
     int steps = s.F / 32;
     if (s.S > 0 && s.Fs / 32 < steps) steps = s.Fs / 32;
+    const long long kmax = (s.S > 0 && s.Fs > s.F) ? s.Fs : s.F;
+    const long long weights = (groups_r * s.F + (long long)s.S * s.Fs) * s.H;  // elements, worst case
+    auto balanced = [&](int ks) { return groups * (s.H / 64) * ks >= 512 && 64 * kmax / ks * 400 <= weights; };
     int ks = 1;
-    while (ks < 16 && (long long)groups * (s.H / 64) * ks < 2048 && steps / (ks * 2) >= 16) ks *= 2;  // ks <= 16
+    while (ks < 16 && !balanced(ks) && steps / (ks * 2) >= 16) ks *= 2;
     return ks;
 }
 
