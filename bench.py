@@ -344,6 +344,9 @@ def main() -> int:
             assert hip.hipEventElapsedTime(ctypes.byref(f), ev_all[i][j], ev_all[i][j + 1]) == 0
             stage_ms[i, j] = f.value
     stage_us = {n: float(stage_ms[:, j].mean() * 1e3) for j, n in enumerate(STAGES)}
+    step_us = stage_ms.sum(axis=1) * 1e3       # per instrumented step: first to last stage event
+    step_pct = {"p10": float(np.percentile(step_us, 10)), "median": float(np.median(step_us)),
+                "p90": float(np.percentile(step_us, 90)), "steps": int(n_diag)}
     t1 = time.perf_counter()
     for i in range(args.steps):
         moe.moe_layer_forward(plain[i % len(plain)], dev.ws, stream)
@@ -356,6 +359,8 @@ def main() -> int:
     ms_per_step = wall * 1e3 / args.steps
     tokens_per_s = cfg.tokens / (ms_per_step * 1e-3)
     p1_us = float(p1_ms.mean() * 1e3)
+    p1_pct = {"p10": float(np.percentile(p1_ms, 10) * 1e3), "median": float(np.median(p1_ms) * 1e3),
+              "p90": float(np.percentile(p1_ms, 90) * 1e3)}
     p1_s = p1_us * 1e-6
     traffic = read_traffic(args.workload)
     if cfg.tokens > 64:
@@ -367,12 +372,14 @@ def main() -> int:
                     "frac": achieved / MFMA_BF16_PEAK_TFLOPS, "traffic": traffic,
                     "algorithmic_flops_per_launch": alg["phase1_flops"],
                     "algorithmic_bytes_per_launch": alg["phase1_bytes"],
-                    "hbm_frac_algorithmic": alg["phase1_bytes"] / p1_s / 1e9 / HBM_PEAK_GBPS, "mean_launch_us": p1_us}
+                    "hbm_frac_algorithmic": alg["phase1_bytes"] / p1_s / 1e9 / HBM_PEAK_GBPS, "mean_launch_us": p1_us,
+                    "launch_us": p1_pct}
     else:
         achieved = alg["phase1_bytes"] / p1_s / 1e9
         roofline = {"kernel": "k_ffn_stream (phase 1: gate/up projections + SwiGLU)", "bound": "hbm",
                     "achieved": achieved, "peak": HBM_PEAK_GBPS, "unit": "GB/s", "frac": achieved / HBM_PEAK_GBPS,
-                    "traffic": traffic, "algorithmic_bytes_per_launch": alg["phase1_bytes"], "mean_launch_us": p1_us}
+                    "traffic": traffic, "algorithmic_bytes_per_launch": alg["phase1_bytes"], "mean_launch_us": p1_us,
+                    "launch_us": p1_pct}
     result = {
         "metric": METRIC,
         "value": tokens_per_s,
@@ -395,6 +402,7 @@ def main() -> int:
         "hbm_gbps_expert_weights": alg["expert_weight_bytes"] / (ms_per_step * 1e-3) / 1e9,
         "hbm_gbps_layer_algorithmic": alg["layer_bytes"] / (ms_per_step * 1e-3) / 1e9,
         "stages_us_instrumented": stage_us,
+        "step_us_instrumented": step_pct,
         "ms_per_step_without_events": ms_no_events,
         "mfma_tflops_layer_algorithmic": alg["flops"] / (ms_per_step * 1e-3) / 1e12,
         "roofline": roofline,

@@ -285,6 +285,33 @@ def test_layer_c6_qwen3_decode(moe, seed):
     run_and_check_layer(moe, SyntheticLayer(CONFIGS["c6_qwen3_decode"], seed))
 
 
+def test_layer_calls_share_one_workspace(moe):
+    """Decode calls of two different layers alternate on one workspace that starts
+    filled with garbage: every call's routing and repack match its own oracle (no
+    state carries over between calls through the workspace)."""
+    from paper_2608_21614_amd.device import DeviceLayer
+    lays = [make_layer(48, 256, 60, 128, 4, dtype="bf16", shared=1, shared_ffn=128, n_resident=30,
+                       residency="random", bias="zipf", seed=s) for s in (21, 22)]
+    devs = [DeviceLayer(l) for l in lays]
+    ws = torch.full_like(devs[0].ws, 0x5A)
+    outs = [d.alloc_outputs() for d in devs]
+    for it in range(3):
+        for lay, dev, o in zip(lays, devs, outs):
+            say("shared workspace: call", it, "seed", lay.seed)
+            dev.ws = ws
+            dev.forward(o)
+            torch.cuda.synchronize()
+            lg_ref = oracle.router_logits(lay.x, lay.w_router, lay.bias)
+            idx = _host(o["topk_idx"])
+            exp_idx, _ = expected_routing(lg_ref, idx, lay.cfg.top_k)
+            np.testing.assert_array_equal(idx, exp_idx)
+            ref = oracle.repack(exp_idx, lay.resident)
+            np.testing.assert_array_equal(_host(o["counts"]), ref["counts"])
+            np.testing.assert_array_equal(_host(o["perm"]), ref["perm"])
+            np.testing.assert_array_equal(_host(o["inv_perm"]), ref["inv_perm"])
+            assert int(_host(o["n_res"])[0]) == ref["n_res"]
+
+
 def test_layer_c4_prefill_sampled(moe):
     say("layer c4_prefill seed 0 (sampled tokens)")
     lay = SyntheticLayer(CONFIGS["c4_prefill"], 0)
