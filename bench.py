@@ -98,9 +98,25 @@ def cpu_baseline(layer, seconds: float):
         if el >= seconds:
             break
     toks = reps * layer.cfg.tokens
-    return {"value": toks / el, "unit": "tokens/s", "cores": oracle.threads(), "kind": "oracle",
+    n = oracle.threads()
+    # one batch on one thread as well (the oracle's results do not depend on the thread count)
+    oracle.set_threads(1)
+    t1 = time.perf_counter()
+    oracle.layer_forward_synthetic(layer, offloaded=False)
+    el1 = time.perf_counter() - t1
+    oracle.set_threads(n)
+    model = "unknown"
+    try:
+        with open("/proc/cpuinfo") as f:
+            model = next((l.split(":", 1)[1].strip() for l in f if l.startswith("model name")), model)
+    except OSError:
+        pass
+    return {"value": toks / el, "unit": "tokens/s", "cores": n, "kind": "oracle",
             "sample": f"{reps} full batch(es) of {layer.cfg.tokens} tokens of the same layer (resident experts + "
-                      f"router + repack, fp64 C with OpenMP), {el:.1f} s"}
+                      f"router + repack, fp64 C with OpenMP), {el:.1f} s",
+            "single_thread": {"value": layer.cfg.tokens / el1, "unit": "tokens/s",
+                              "sample": f"1 batch of {layer.cfg.tokens} tokens, {el1:.1f} s"},
+            "cpu_model": model, "logical_cpus_visible": os.cpu_count()}
 
 
 # rates of this machine (MI355X machine, 16 host threads): host->device copies, the host FFN on

@@ -68,6 +68,8 @@ def _load():
         lib.oracle_expert_ffn.restype = None
         lib.oracle_threads.argtypes = []
         lib.oracle_threads.restype = ctypes.c_int
+        lib.oracle_set_threads.argtypes = [ctypes.c_int]
+        lib.oracle_set_threads.restype = None
         _lib = lib
     return _lib
 
@@ -75,6 +77,11 @@ def _load():
 def threads() -> int:
     """OpenMP threads the oracle's loops run on."""
     return int(_load().oracle_threads())
+
+
+def set_threads(n: int) -> None:
+    """Threads for later calls (results do not depend on it: loops split outputs, not sums)."""
+    _load().oracle_set_threads(int(n))
 
 
 def _ptr(a: Optional[np.ndarray]):

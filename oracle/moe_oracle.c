@@ -52,6 +52,10 @@ int oracle_version(void) { return 1; }
 /* Threads the OpenMP loops below use. */
 int oracle_threads(void) { return omp_get_max_threads(); }
 
+/* Threads for the following calls; every loop splits outputs, never a sum, so the
+ * results do not depend on it. */
+void oracle_set_threads(int n) { omp_set_num_threads(n > 0 ? n : 1); }
+
 /*
  * Router scores (Section II-A): score[t][e] = sum_h x[t][h] * w_router[e][h] + bias[e].
  * x is [T,H], w_router is [E,H] (row e scores expert e), bias is [E] fp32 or NULL.

@@ -373,6 +373,22 @@ def test_layer_sampled_tokens_match_full_batch():
     np.testing.assert_array_equal(samp["out_off"], full["out_off"][[11, 0, 5]])
 
 
+def test_layer_independent_of_thread_count():
+    """The oracle's loops split outputs, never sums: one thread gives the same bits."""
+    lay = make_layer(24, 128, 8, 128, 2, dtype="bf16", shared=1, shared_ffn=64, n_resident=5, residency="random",
+                     seed=4)
+    n = oracle.threads()
+    try:
+        a = oracle.layer_forward_synthetic(lay, offloaded=True)
+        oracle.set_threads(1)
+        assert oracle.threads() == 1
+        b = oracle.layer_forward_synthetic(lay, offloaded=True)
+    finally:
+        oracle.set_threads(n)
+    for key in ("out_res", "out_off", "perm", "counts"):
+        np.testing.assert_array_equal(a[key], b[key])
+
+
 def test_layer_given_logits_and_selection():
     lay = make_layer(tokens=4, hidden=8, experts=4, ffn=8, top_k=2, dtype="f32", seed=15)
     g = json.load(open(os.path.join(GOLDEN, "repack_worked_example.json")))
