@@ -28,7 +28,9 @@ def say(*a):
     print("[case]", *a, flush=True)
 
 
-def test_stage_trace_residency_and_chr(moe):
+@pytest.fixture(scope="module")
+def trace_run(moe):
+    """The whole trace on the GPU (routing, logs, plans) and the oracle's counts and replay."""
     from paper_2608_21614_amd.stage_trace import run_routing_trace
     cfg = TRACE
     trace = StageTrace(cfg, seed=0)
@@ -52,40 +54,57 @@ def test_stage_trace_residency_and_chr(moe):
         for s in range(cfg.steps):
             counts[s, l] = oracle.repack(exp_idx[s * T:(s + 1) * T], np.ones(E, bool))["counts"]
         say(f"layer {l}: routing exact ({len(alts)} near-tied tokens)")
-    np.testing.assert_array_equal(gpu["counts"], counts)
 
     init = np.full((L, E), -1, np.int32)
     for l in range(L):
         ids = np.flatnonzero(trace.initial_resident[l])
         init[l, ids] = np.arange(len(ids))
     ref = oracle.stage_replay(counts, trace.stage_len, init, cfg.n_slots)
+    return {"trace": trace, "xs": xs, "gpu": gpu, "counts": counts, "ref": ref, "stage_of": stage_of}
+
+
+def test_stage_trace_residency_and_chr(trace_run):
+    gpu, counts, ref = trace_run["gpu"], trace_run["counts"], trace_run["ref"]
+    np.testing.assert_array_equal(gpu["counts"], counts)
     np.testing.assert_array_equal(gpu["slot_history"], ref["slot_history"])
     res_pairs = (counts * ref["resident"]).sum(axis=2)
     np.testing.assert_array_equal(gpu["n_res"], res_pairs)
     assert gpu["chr_online"] == ref["chr_online"]
     say(f"CHR online {ref['chr_online']:.4f}, clairvoyant {ref['chr_clairvoyant']:.4f}, eta {ref['eta_chr']:.4f}")
 
-    # full layer forward on sampled calls, with the residency in effect at that step
+
+def test_stage_trace_forward_first_and_last_step_of_every_stage(trace_run):
+    """The full layer forward (resident partial) at the first and the last step of
+    every stage, for the first and the last layer, with the residency in effect at
+    that step; the FFN output is checked on sampled tokens."""
     from paper_2608_21614_amd.device import DeviceLayer, to_host
-    ends = trace.stage_ends()
-    for step, l in [(0, 0), (int(ends[0]), 7), (cfg.steps - 1, 3)]:
-        s = int(stage_of[step])
-        say(f"forward at step {step} layer {l} stage {s}")
-        lay = SyntheticLayer(cfg.layer_config(), 0, layer=l)
-        lay.x = xs[l][step]
-        lay.bias = trace.stage_bias[s, l].copy()
-        slot = ref["slot_history"][s, l]
-        lay.set_residency(slot >= 0, expert_slot=slot)
-        dev = DeviceLayer(lay)
-        o = dev.alloc_outputs()
-        dev.forward(o)
-        torch.cuda.synchronize()
-        idx = to_host(o["topk_idx"])
-        np.testing.assert_array_equal(idx, gpu["topk_idx"][step, l])
-        out = oracle.layer_forward_synthetic(lay, idx=idx, offloaded=False)
-        np.testing.assert_array_equal(to_host(o["counts"]), out["counts"])
-        err = rel_l2(host_f64(o["out"]), out["out_res"])
-        say(f"  rel-L2 {err:.3e}")
-        assert err <= TOL["bf16"]
-        del dev, lay
+    cfg = TRACE
+    trace, xs, gpu, ref, stage_of = (trace_run[n] for n in ("trace", "xs", "gpu", "ref", "stage_of"))
+    ends = [int(v) for v in trace.stage_ends()]
+    firsts = [0] + [e + 1 for e in ends[:-1]]
+    sample = np.array([0, cfg.batch // 2, cfg.batch - 1])
+    for l in (0, cfg.layers - 1):
+        lay = SyntheticLayer(cfg.layer_config(), 0, layer=l)      # expert weights cached across the calls
+        for s in range(trace.n_stages):
+            for step in sorted({firsts[s], ends[s]}):
+                assert int(stage_of[step]) == s
+                lay.x = xs[l][step]
+                lay.bias = trace.stage_bias[s, l].copy()
+                slot = ref["slot_history"][s, l]
+                lay.set_residency(slot >= 0, expert_slot=slot)
+                dev = DeviceLayer(lay)
+                o = dev.alloc_outputs()
+                dev.forward(o)
+                torch.cuda.synchronize()
+                idx = to_host(o["topk_idx"])
+                np.testing.assert_array_equal(idx, gpu["topk_idx"][step, l])
+                out = oracle.layer_forward_synthetic(lay, idx=idx, offloaded=False, sample=sample)
+                np.testing.assert_array_equal(to_host(o["counts"]), out["counts"])
+                assert int(to_host(o["n_res"])[0]) == int(gpu["n_res"][step, l])
+                err = rel_l2(host_f64(o["out"])[sample], out["out_res"])
+                say(f"  layer {l} stage {s} step {step}: resident {np.flatnonzero(slot >= 0).tolist()}, "
+                    f"rel-L2 {err:.3e}")
+                assert err <= TOL["bf16"]
+                del dev, o
+        del lay
         torch.cuda.empty_cache()
