@@ -12,8 +12,8 @@
 // MFMA A operands.
 //
 // Three kernel families:
-//  * stream  (T <= 64, decode; bf16 MFMA 16x16x32, fp32 MFMA 16x16x4): the weights are streamed from HBM exactly
-//    once.  A workgroup owns 32 features (phase 1: 32 gate + 32 up weight
+//  * stream  (T <= 64, decode; bf16 MFMA 16x16x32, fp32 MFMA 16x16x4): the
+//    weights are streamed from HBM exactly once.  A workgroup owns 32 features (phase 1: 32 gate + 32 up weight
 //    rows) or 64 outputs (phase 2: 64 rows of W2) of one expert; the weights are
 //    the MFMA M side and the expert's tokens the N side, in tiles of 16.  Its
 //    four waves split K interleaved -- wave w takes the 32-wide K steps w, w+4,
@@ -25,8 +25,9 @@
 //    adds in fixed order.  SwiGLU is applied in the phase-1 epilogue, so the gate
 //    and up projections are never stored.
 //  * tiled   (bf16, T > 64, prefill): workgroup tiles of 128 weight rows x 128
-//    tokens (64 x 64 per wave), K staged through LDS in double-buffered 64-wide
-//    slabs; each phase-1 wave holds the gate and up rows of the same features so
+//    tokens (64 x 64 per wave); K runs in 64-wide slabs through one LDS buffer
+//    while the next slab is loaded into registers, so three workgroups fit on a
+//    CU; each phase-1 wave holds the gate and up rows of the same features so
 //    SwiGLU runs in registers.
 //  * f32     (fp32, T > 64): plain fp32 FMA, one output per thread.
 // All of them read counts and offsets from device memory: the grid is sized for
