@@ -4,7 +4,7 @@
 // reproducible (Section V-C).
 //
 // Workgroup = one token x 1024 hidden columns (4 per thread, 16-byte loads):
-//   acc = 0
+//   acc = 0  (fp32)
 //   for j in 0..k-1:  acc += w[t,j] * (sum_c y[c][inv[t,j]])          resident
 //                     acc += w[t,j] * y_off[inv[t,j] - n_res]          offloaded, if given
 //   for s in 0..S-1:  acc += sum_c y[c][T*k + s*T + t]
@@ -29,34 +29,97 @@ __device__ __forceinline__ f32x4 sum_chunks(const float* __restrict__ y, int ks,
     return v;
 }
 
-template <bool kOutBf16>
+// Workgroup = one token x 1024 columns.  The token's indices (choices, gate
+// weights, packed rows, residency) are loaded first, all at once; then every
+// contribution's loads are issued without branches (a contribution that does
+// not apply reads a valid row and is replaced by zero, never multiplied by it);
+// then the sums run in the fixed order above.  KS >= ks is the compile-time
+// bound on the K chunks; above two chunks the loads go one contribution at a
+// time (all of its chunks together), which keeps the registers in bounds.
+template <bool kOutBf16, int KS>
 __global__ void __launch_bounds__(256)
     k_combine(int T, int H, int E, int k, int S, int slots, const int32_t* __restrict__ topk_idx,
               const float* __restrict__ topk_w, const int32_t* __restrict__ inv_perm,
               const int32_t* __restrict__ expert_slot, const float* __restrict__ y, int ks, long long stride,
               const float* __restrict__ y_off, const int32_t* __restrict__ n_res_p, void* __restrict__ out) {
+    constexpr int kK = 8, kS = 8;  // bounds on k and S (the ABI checks both)
     const int t = blockIdx.x;
     const int h = (blockIdx.y * 256 + threadIdx.x) * 4;
     if (h >= H) return;
     const int P = T * k;
     const int nres = y_off ? *n_res_p : 0;
-    f32x4 acc = {0.f, 0.f, 0.f, 0.f};
-    for (int j = 0; j < k; ++j) {
-        const int q = t * k + j;
-        const int e = topk_idx[q];
-        if (e < 0 || e >= E) continue;
-        const int p = inv_perm[q];
-        if (p < 0 || p >= P) continue;
-        const float w = topk_w[q];
-        if (is_resident(expert_slot[e], slots)) {
-            acc += w * sum_chunks(y, ks, stride, (size_t)p * H + h);
-        } else if (y_off && p >= nres) {
-            acc += w * *reinterpret_cast<const f32x4*>(y_off + (size_t)(p - nres) * H + h);
+
+    // the token's choices
+    int e[kK], p[kK];
+    float w[kK];
+#pragma unroll
+    for (int j = 0; j < kK; ++j) {
+        e[j] = -1;
+        p[j] = -1;
+        w[j] = 0.f;
+        if (j < k) {
+            e[j] = topk_idx[t * k + j];
+            p[j] = inv_perm[t * k + j];
+            w[j] = topk_w[t * k + j];
         }
     }
-    for (int s = 0; s < S; ++s) {
-        const size_t row = (size_t)P + (size_t)s * T + t;
-        acc += sum_chunks(y, ks, stride, row * H + h);
+    // where each choice's row lives: 1 = y (resident), 2 = y_off (offloaded, given), 0 = nowhere
+    int src[kK];
+#pragma unroll
+    for (int j = 0; j < kK; ++j) {
+        src[j] = 0;
+        if (j < k && e[j] >= 0 && e[j] < E && p[j] >= 0 && p[j] < P) {
+            if (is_resident(expert_slot[e[j]], slots)) src[j] = 1;
+            else if (y_off && p[j] >= nres) src[j] = 2;
+        }
+    }
+    const f32x4 zero = {0.f, 0.f, 0.f, 0.f};
+    f32x4 acc = zero;
+    if constexpr (KS <= 2) {
+        // every contribution's loads at once, then the fixed-order sums
+        f32x4 v[kK][KS], vs[kS][KS];
+#pragma unroll
+        for (int j = 0; j < kK; ++j) {
+            const size_t off = (size_t)(src[j] ? p[j] : 0) * H + h;
+            const float* base = (src[j] == 2) ? y_off + (off - (size_t)nres * H) : y + off;
+#pragma unroll
+            for (int c = 0; c < KS; ++c) {
+                const bool use = src[j] == 1 ? c < ks : (src[j] == 2 && c == 0);
+                const f32x4 l = *reinterpret_cast<const f32x4*>(base + (use ? c * stride : 0));
+                v[j][c] = use ? l : zero;
+            }
+        }
+#pragma unroll
+        for (int s2 = 0; s2 < kS; ++s2) {
+            const size_t off = (size_t)(s2 < S ? P + s2 * T + t : 0) * H + h;
+#pragma unroll
+            for (int c = 0; c < KS; ++c) {
+                const bool use = s2 < S && c < ks;
+                const f32x4 l = *reinterpret_cast<const f32x4*>(y + off + (use ? c * stride : 0));
+                vs[s2][c] = use ? l : zero;
+            }
+        }
+#pragma unroll
+        for (int j = 0; j < kK; ++j) {
+            if (!src[j]) continue;  // uniform over the workgroup
+            f32x4 r = v[j][0];
+            if (KS > 1 && src[j] == 1 && ks > 1) r += v[j][KS - 1];
+            acc += w[j] * r;
+        }
+#pragma unroll
+        for (int s2 = 0; s2 < kS; ++s2) {
+            if (s2 >= S) continue;
+            f32x4 r = vs[s2][0];
+            if (KS > 1 && ks > 1) r += vs[s2][KS - 1];
+            acc += r;
+        }
+    } else {
+        // one contribution at a time, its chunk loads together
+        for (int j = 0; j < k; ++j) {
+            if (src[j] == 1) acc += w[j] * sum_chunks(y, ks, stride, (size_t)p[j] * H + h);
+            else if (src[j] == 2) acc += w[j] * *reinterpret_cast<const f32x4*>(y_off + (size_t)(p[j] - nres) * H + h);
+        }
+        for (int s2 = 0; s2 < S; ++s2) acc += sum_chunks(y, ks, stride, ((size_t)P + (size_t)s2 * T + t) * H + h);
     }
     if (kOutBf16) {
         u32x2 packed;
@@ -73,20 +136,32 @@ __global__ void k_stage_accumulate(int E, const int32_t* __restrict__ counts, in
     if (e < E) log[e] += counts[e];
 }
 
+template <bool kOutBf16>
+hipError_t launch_combine_ks(dim3 grid, const Shape& s, const int32_t* topk_idx, const float* topk_w,
+                             const int32_t* inv_perm, const int32_t* expert_slot, const float* y, int ks,
+                             long long stride, const float* y_off, const int32_t* n_res, void* out, hipStream_t st) {
+#define SAEM_COMBINE(KS)                                                                                            \
+    hipLaunchKernelGGL((k_combine<kOutBf16, KS>), grid, dim3(256), 0, st, s.T, s.H, s.E, s.k, s.S, s.slots,      \
+                       topk_idx, topk_w, inv_perm, expert_slot, y, ks, stride, y_off, n_res, out)
+    if (ks <= 1) SAEM_COMBINE(1);
+    else if (ks <= 2) SAEM_COMBINE(2);
+    else SAEM_COMBINE(16);
+#undef SAEM_COMBINE
+    return hipGetLastError();
+}
+
 }  // namespace
 
 hipError_t launch_combine(const Shape& s, const int32_t* topk_idx, const float* topk_w, const int32_t* inv_perm,
                           const int32_t* expert_slot, const float* y, int ks, long long y_ks_stride,
                           const float* y_off, const int32_t* n_res, void* out, bool out_bf16, hipStream_t st) {
     if (s.T == 0) return hipSuccess;
-    dim3 grid(s.T, (s.H + 1023) / 1024), block(256);
-    if (out_bf16)
-        hipLaunchKernelGGL(k_combine<true>, grid, block, 0, st, s.T, s.H, s.E, s.k, s.S, s.slots, topk_idx, topk_w,
-                           inv_perm, expert_slot, y, ks, y_ks_stride, y_off, n_res, out);
-    else
-        hipLaunchKernelGGL(k_combine<false>, grid, block, 0, st, s.T, s.H, s.E, s.k, s.S, s.slots, topk_idx, topk_w,
-                           inv_perm, expert_slot, y, ks, y_ks_stride, y_off, n_res, out);
-    return hipGetLastError();
+    if (ks < 1 || ks > 16 || s.k > 8 || s.S > 8) return hipErrorInvalidValue;
+    const dim3 grid(s.T, (s.H + 1023) / 1024);
+    return out_bf16 ? launch_combine_ks<true>(grid, s, topk_idx, topk_w, inv_perm, expert_slot, y, ks, y_ks_stride,
+                                              y_off, n_res, out, st)
+                    : launch_combine_ks<false>(grid, s, topk_idx, topk_w, inv_perm, expert_slot, y, ks, y_ks_stride,
+                                               y_off, n_res, out, st);
 }
 
 hipError_t launch_stage_accumulate(int E, const int32_t* counts, int64_t* log, hipStream_t st) {
