@@ -94,41 +94,53 @@ struct Group {
 };
 
 // Active resident routed experts (ascending id) into s_list; returns their number.
+// With s_info, entry i also gets expert s_list[i]'s (segment start, count, slot),
+// read in the same round trip as the counts.
 // Must be called by all threads of a 256-thread workgroup.
-__device__ int list_active(const Args& a, int* s_list, int* s_wsum) {
+__device__ int list_active(const Args& a, int* s_list, int* s_wsum, int4* s_info = nullptr) {
     const int tid = threadIdx.x, wave = tid >> 6, lane = lane_id();
     const int e = tid;
     bool act = false;
+    int sl = -1, cnt = 0, seg = 0;
     if (e < a.E) {
-        const int sl = a.expert_slot[e];
-        act = is_resident(sl, a.slots) && a.counts[e] > 0;
+        sl = a.expert_slot[e];
+        cnt = a.counts[e];
+        if (s_info) seg = a.seg_start[e];
+        act = is_resident(sl, a.slots) && cnt > 0;
     }
     const unsigned long long b = __ballot(act);
     if (lane == 0) s_wsum[wave] = __popcll(b);
     __syncthreads();
     int base = 0;
     for (int w = 0; w < wave; ++w) base += s_wsum[w];
-    if (act) s_list[base + __popcll(b & ((1ull << lane) - 1ull))] = e;
+    if (act) {
+        const int pos = base + __popcll(b & ((1ull << lane) - 1ull));
+        s_list[pos] = e;
+        if (s_info) s_info[pos] = make_int4(seg, cnt, sl, 0);
+    }
     const int n = s_wsum[0] + s_wsum[1] + s_wsum[2] + s_wsum[3];
     __syncthreads();
     return n;
 }
 
-__device__ Group routed_group(const Args& a, int e, size_t elt) {
+// Routed group from its expert's segment start, count and slot.
+__device__ Group routed_group_of(const Args& a, int rb, int c, int slot_, size_t elt) {
     Group g;
     const int P = a.T * a.k;
-    int rb = a.seg_start[e];
-    int c = a.counts[e];
     rb = rb < 0 ? 0 : (rb > P ? P : rb);
     c = c < 0 ? 0 : (c > P - rb ? P - rb : c);
     g.rowbase = rb;
     g.count = c;
     g.routed = 1;
     g.Fg = a.F;
-    const size_t slot = (size_t)a.expert_slot[e];
+    const size_t slot = (size_t)slot_;
     g.w13 = static_cast<const uint8_t*>(a.w13) + slot * 2 * a.F * a.H * elt;
     g.w2 = static_cast<const uint8_t*>(a.w2) + slot * a.H * a.F * elt;
     return g;
+}
+
+__device__ Group routed_group(const Args& a, int e, size_t elt) {
+    return routed_group_of(a, a.seg_start[e], a.counts[e], a.expert_slot[e], elt);
 }
 
 __device__ Group shared_group(const Args& a, int s, size_t elt) {
@@ -166,6 +178,7 @@ __global__ void __launch_bounds__(256) k_ffn_stream(Args a) {
     constexpr int U = sizeof(Elt) == 2 ? 2 : 1;    // K steps per load batch (two batches in flight)
     __shared__ int s_list[256];
     __shared__ int s_wsum[4];
+    __shared__ int4 s_info[256];
     __shared__ f32x4 s_red[4][MT][NT][kWave];
 
     const int item = blockIdx.x;
@@ -174,7 +187,7 @@ __global__ void __launch_bounds__(256) k_ffn_stream(Args a) {
         pack_offloaded(a, item - n_items, gridDim.x - n_items, sizeof(Elt));
         return;
     }
-    const int nact = list_active(a, s_list, s_wsum);
+    const int nact = list_active(a, s_list, s_wsum, s_info);
     // shared groups first: their items can be longer (Fs > F in phase 2), so they
     // start in the first wave of workgroups instead of forming a tail
     Group g;
@@ -186,7 +199,8 @@ __global__ void __launch_bounds__(256) k_ffn_stream(Args a) {
         const int i2 = item - a.S * a.ipg_s;
         const int gi = i2 / a.ipg_r;
         if (gi >= nact) return;
-        g = routed_group(a, s_list[gi], sizeof(Elt));
+        const int4 info = s_info[gi];
+        g = routed_group_of(a, info.x, info.y, info.z, sizeof(Elt));
         sub = i2 % a.ipg_r;
     }
     if (g.count == 0) return;
