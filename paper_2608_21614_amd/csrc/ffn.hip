@@ -238,6 +238,20 @@ __global__ void __launch_bounds__(256) k_ffn_stream(Args a) {
     const int n_my = (c1 - c0 > wave) ? (c1 - c0 - wave + 3) / 4 : 0;
     const int sbase = c0 + wave;
 
+    const int nb = n_my / U;
+    // batch b holds this wave's steps i = U*b .. U*b+U-1
+    auto load_w = [&](F8 (&A)[U][MT], int b) {
+#pragma unroll
+        for (int u = 0; u < U; ++u) {
+            const int s = sbase + 4 * (U * b + u);
+#pragma unroll
+            for (int m = 0; m < MT; ++m) A[u][m] = load_frag(wp[m] + (size_t)s * 512);
+        }
+    };
+    // the first batch's weights go out before the token rows are looked up
+    F8 A0[U][MT], B0[U][NT], A1[U][MT], B1[U][NT];
+    if (nb > 0) load_w(A0, 0);
+
     // token operand rows (N side)
     const int ntile = min(NT, (g.count + 15) / 16);
     const Elt* bp[NT];
@@ -259,16 +273,17 @@ __global__ void __launch_bounds__(256) k_ffn_stream(Args a) {
 #pragma unroll
         for (int j = 0; j < NT; ++j) acc[m][j] = f32x4{0.f, 0.f, 0.f, 0.f};
 
-    // batch b holds this wave's steps i = U*b .. U*b+U-1
-    auto load = [&](F8 (&A)[U][MT], F8 (&B)[U][NT], int b) {
+    auto load_x = [&](F8 (&B)[U][NT], int b) {
 #pragma unroll
         for (int u = 0; u < U; ++u) {
             const int s = sbase + 4 * (U * b + u);
 #pragma unroll
-            for (int m = 0; m < MT; ++m) A[u][m] = load_frag(wp[m] + (size_t)s * 512);
-#pragma unroll
             for (int j = 0; j < NT; ++j) B[u][j] = (j < ntile && bp[j]) ? load_frag(bp[j] + s * 32) : zero_frag<Elt>();
         }
+    };
+    auto load = [&](F8 (&A)[U][MT], F8 (&B)[U][NT], int b) {
+        load_w(A, b);
+        load_x(B, b);
     };
     auto mma = [&](const F8 (&A)[U][MT], const F8 (&B)[U][NT]) {
         // tiles past the group's last token see zero operands: no branch, fewer live registers
@@ -279,10 +294,8 @@ __global__ void __launch_bounds__(256) k_ffn_stream(Args a) {
 #pragma unroll
                 for (int m = 0; m < MT; ++m) acc[m][j] = mma_frag(A[u][m], B[u][j], acc[m][j]);
     };
-    const int nb = n_my / U;
     {
-        F8 A0[U][MT], B0[U][NT], A1[U][MT], B1[U][NT];
-        if (nb > 0) load(A0, B0, 0);
+        if (nb > 0) load_x(B0, 0);
         for (int b = 0; b < nb; b += 2) {
             if (b + 1 < nb) load(A1, B1, b + 1);
             mma(A0, B0);
