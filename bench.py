@@ -369,6 +369,20 @@ def main() -> int:
     torch.cuda.synchronize()
     ms_no_events = (time.perf_counter() - t1) * 1e3 / args.steps
 
+    # streaming-read reference of this GPU: one pass of 16-byte loads over 4 GiB
+    probe_src = torch.empty(1 << 30, dtype=torch.float32, device="cuda")
+    probe_sink = torch.zeros(1, dtype=torch.int32, device="cuda")
+    pe0, pe1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    for _ in range(2):
+        moe.moe_read_probe(probe_src, probe_sink, stream=stream)
+    pe0.record(stream)
+    for _ in range(10):
+        moe.moe_read_probe(probe_src, probe_sink, stream=stream)
+    pe1.record(stream)
+    torch.cuda.synchronize()
+    read_probe_gbps = 10 * probe_src.numel() * 4 / (pe0.elapsed_time(pe1) * 1e-3) / 1e9
+    del probe_src, probe_sink
+
     counts = to_host(o["counts"])
     resident = (layer.expert_slot >= 0) & (layer.expert_slot < dev.slots)
     alg = algorithmic_bytes(cfg, counts, resident)
@@ -394,6 +408,7 @@ def main() -> int:
         achieved = alg["phase1_bytes"] / p1_s / 1e9
         roofline = {"kernel": "k_ffn_stream (phase 1: gate/up projections + SwiGLU)", "bound": "hbm",
                     "achieved": achieved, "peak": HBM_PEAK_GBPS, "unit": "GB/s", "frac": achieved / HBM_PEAK_GBPS,
+                    "read_probe_GBps": read_probe_gbps, "frac_of_read_probe": achieved / read_probe_gbps,
                     "traffic": traffic, "algorithmic_bytes_per_launch": alg["phase1_bytes"], "mean_launch_us": p1_us,
                     "launch_us": p1_pct}
     result = {
@@ -420,6 +435,7 @@ def main() -> int:
         "stages_us_instrumented": stage_us,
         "step_us_instrumented": step_pct,
         "ms_per_step_without_events": ms_no_events,
+        "hbm_read_probe_GBps": read_probe_gbps,
         "mfma_tflops_layer_algorithmic": alg["flops"] / (ms_per_step * 1e-3) / 1e12,
         "roofline": roofline,
     }

@@ -310,6 +310,17 @@ typedef struct moe_offload_rates {
 moe_status moe_offload_plan(int32_t experts, const int32_t* counts, const int32_t* expert_slot, int32_t slots,
                             const moe_offload_rates* rates, int32_t max_copies, int32_t* choice);
 
+/*
+ * Measurement utility (not a step of the method): reads `bytes` of device
+ * memory at src once, with 16-byte loads spread over the whole GPU, so that the
+ * caller can time the streaming-read rate of this GPU's HBM on its stream and
+ * compare the weight-streaming FFN against it.
+ *   src: device, 16-byte aligned; bytes >= 0, a multiple of 16.
+ *   sink: device, one uint32 that is left unchanged in practice (a store
+ *   conditioned on the data keeps the loads from being removed).
+ */
+moe_status moe_read_probe(const void* src, int64_t bytes, uint32_t* sink, void* stream);
+
 #ifdef __cplusplus
 }
 #endif

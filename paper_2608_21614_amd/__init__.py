@@ -26,7 +26,7 @@ MOE_HOST_PIN = 1
 EXPORTED = [
     "moe_abi_version", "moe_status_str", "moe_check_dims", "moe_workspace_bytes", "moe_route_topk",
     "moe_repack", "moe_grouped_ffn", "moe_combine", "moe_layer_forward", "moe_stage_accumulate",
-    "moe_stage_plan", "moe_pack_weights", "moe_host_ffn", "moe_offload_plan",
+    "moe_stage_plan", "moe_pack_weights", "moe_host_ffn", "moe_offload_plan", "moe_read_probe",
 ]
 
 
@@ -108,6 +108,7 @@ def _load() -> ctypes.CDLL:
         "moe_host_ffn": ([D, _vp, _vp, i32, ctypes.POINTER(_vp), ctypes.POINTER(_vp), _vp, _vp, i32, u32],
                          ctypes.c_int),
         "moe_offload_plan": ([i32, _vp, _vp, i32, ctypes.POINTER(moe_offload_rates), i32, _vp], ctypes.c_int),
+        "moe_read_probe": ([_vp, ctypes.c_int64, _vp, _vp], ctypes.c_int),
     }
     for name, (args, res) in sig.items():
         fn = getattr(lib, name)
@@ -215,6 +216,13 @@ def moe_pack_weights(src, dst, stream=None):
 
 def moe_stage_accumulate(experts: int, counts, log, stream=None):
     _check(lib.moe_stage_accumulate(int(experts), _p(counts), _p(log), _stream(stream)), "moe_stage_accumulate")
+
+
+def moe_read_probe(src, sink, nbytes=None, stream=None):
+    """One pass of 16-byte loads over the device tensor `src` (a measurement utility:
+    time it on `stream` to get this GPU's streaming-read rate); sink: 1 int32 on the device."""
+    n = src.numel() * src.element_size() if nbytes is None else int(nbytes)
+    _check(lib.moe_read_probe(_p(src), n, _p(sink), _stream(stream)), "moe_read_probe")
 
 
 def moe_host_ffn(dims, counts, seg_start, n_res: int, w13_host, w2_host, off_rows, y_off=None, threads: int = 0,

@@ -14,7 +14,7 @@ HERE = os.path.dirname(os.path.abspath(__file__))
 CSRC = os.path.join(HERE, "csrc")
 LIB = os.path.join(HERE, "libsaem_moe.so")
 BUILD_DIR = os.path.join(HERE, "_build")
-SOURCES = ["abi.hip", "route.hip", "repack.hip", "ffn.hip", "combine.hip", "pack.hip"]
+SOURCES = ["abi.hip", "route.hip", "repack.hip", "ffn.hip", "combine.hip", "pack.hip", "probe.hip"]
 HOST_SOURCES = ["host_ffn.cpp"]   # host-only C++ (system compiler)
 ARCH = "gfx950"
 

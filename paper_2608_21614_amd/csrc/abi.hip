@@ -304,6 +304,11 @@ moe_status moe_stage_accumulate(int32_t experts, const int32_t* counts, int64_t*
     return hip_status(saem::launch_stage_accumulate(experts, counts, log, static_cast<hipStream_t>(stream)));
 }
 
+moe_status moe_read_probe(const void* src, int64_t bytes, uint32_t* sink, void* stream) {
+    if (bytes < 0 || bytes % 16 != 0 || (bytes > 0 && !ok_ptr(src)) || !ok_ptr4(sink)) return MOE_ERR_INVALID_ARG;
+    return hip_status(saem::launch_read_probe(src, bytes, sink, static_cast<hipStream_t>(stream)));
+}
+
 moe_status moe_stage_plan(int32_t experts, int32_t slots, const int64_t* log, const int32_t* prev_slot,
                           int32_t* new_slot) {
     if (experts <= 0 || experts > 256 || slots < 0 || slots > experts || !log || !prev_slot || !new_slot)

@@ -76,4 +76,7 @@ hipError_t launch_pack_weights(const void* src, void* dst, long long rows, long 
 
 hipError_t launch_stage_accumulate(int E, const int32_t* counts, int64_t* log, hipStream_t st);
 
+// Measurement utility: one pass of 16-byte loads over `bytes` of src (a multiple of 16).
+hipError_t launch_read_probe(const void* src, long long bytes, uint32_t* sink, hipStream_t st);
+
 }  // namespace saem

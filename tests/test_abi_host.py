@@ -141,6 +141,12 @@ def test_invalid_pointers_rejected_before_any_launch(pkg):
     # stage accumulate
     assert lib.moe_stage_accumulate(0, f, f, None) == 1
     assert lib.moe_stage_accumulate(8, None, f, None) == 1
+    # read probe: size not a multiple of 16, negative, missing or misaligned buffers
+    assert lib.moe_read_probe(f, 100, f, None) == 1
+    assert lib.moe_read_probe(f, -16, f, None) == 1
+    assert lib.moe_read_probe(None, 1024, f, None) == 1
+    assert lib.moe_read_probe(_fake(0x10008), 1024, f, None) == 1
+    assert lib.moe_read_probe(f, 1024, None, None) == 1
 
 
 def test_layer_forward_struct_checks(pkg):

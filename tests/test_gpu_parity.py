@@ -442,3 +442,15 @@ def test_stage_accumulate(moe):
     moe.moe_stage_accumulate(4, counts, log)
     torch.cuda.synchronize()
     np.testing.assert_array_equal(_host(log), [16, 20, 40, 2**40 + 2])
+
+
+def test_read_probe_runs_and_keeps_sink(moe):
+    """The streaming-read probe (a measurement utility) reads a buffer once and leaves the sink alone."""
+    say("read probe")
+    src = torch.zeros(1 << 22, dtype=torch.float32, device="cuda")      # 16 MiB of zeros: the xor is 0
+    sink = torch.full((1,), 7, dtype=torch.int32, device="cuda")
+    moe.moe_read_probe(src, sink)
+    moe.moe_read_probe(src, sink, nbytes=16 * 1001)                       # a ragged tail of chunks
+    moe.moe_read_probe(src, sink, nbytes=0)
+    torch.cuda.synchronize()
+    assert int(sink.item()) == 7
