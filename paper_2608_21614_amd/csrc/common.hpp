@@ -69,6 +69,12 @@ __device__ __forceinline__ Frag8<float> load_frag(const float* p) {
     const f32x4* q = reinterpret_cast<const f32x4*>(p);
     return {q[0], q[1]};
 }
+// Read-once operands (an expert's weights at decode): non-temporal loads.
+__device__ __forceinline__ Frag8<uint16_t> load_frag_stream(const uint16_t* p) { return {load_bf16x8_stream(p)}; }
+__device__ __forceinline__ Frag8<float> load_frag_stream(const float* p) {
+    const f32x4* q = reinterpret_cast<const f32x4*>(p);
+    return {__builtin_nontemporal_load(q), __builtin_nontemporal_load(q + 1)};
+}
 template <typename Elt>
 __device__ __forceinline__ Frag8<Elt> zero_frag();
 template <>

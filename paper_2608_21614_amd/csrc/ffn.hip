@@ -171,7 +171,11 @@ __device__ __forceinline__ int group_token(const Args& a, const Group& g, int n)
 // stream kernel (decode)
 // ---------------------------------------------------------------------------
 
-template <typename Elt, int NT, bool kDown>
+// kStreamW: the weights are loaded non-temporally (they do not stay in the
+// caches for a later use), which raises the streaming rate when the call's
+// weights are far larger than the caches; small weight sets that stay in the
+// MALL between calls are read with plain loads.
+template <typename Elt, int NT, bool kDown, bool kStreamW>
 __global__ void __launch_bounds__(256) k_ffn_stream(Args a) {
     using F8 = Frag8<Elt>;
     constexpr int MT = 4;                          // 16-row weight tiles per workgroup
@@ -245,7 +249,8 @@ __global__ void __launch_bounds__(256) k_ffn_stream(Args a) {
         for (int u = 0; u < U; ++u) {
             const int s = sbase + 4 * (U * b + u);
 #pragma unroll
-            for (int m = 0; m < MT; ++m) A[u][m] = load_frag(wp[m] + (size_t)s * 512);
+            for (int m = 0; m < MT; ++m)
+                A[u][m] = kStreamW ? load_frag_stream(wp[m] + (size_t)s * 512) : load_frag(wp[m] + (size_t)s * 512);
         }
     };
     // the first batch's weights go out before the token rows are looked up
@@ -307,7 +312,8 @@ __global__ void __launch_bounds__(256) k_ffn_stream(Args a) {
         const int s = sbase + 4 * i;
         F8 A[MT], B[NT];
 #pragma unroll
-        for (int m = 0; m < MT; ++m) A[m] = load_frag(wp[m] + (size_t)s * 512);
+        for (int m = 0; m < MT; ++m)
+            A[m] = kStreamW ? load_frag_stream(wp[m] + (size_t)s * 512) : load_frag(wp[m] + (size_t)s * 512);
 #pragma unroll
         for (int j = 0; j < NT; ++j) B[j] = (j < ntile && bp[j]) ? load_frag(bp[j] + s * 32) : zero_frag<Elt>();
 #pragma unroll
@@ -674,14 +680,29 @@ int max_routed_groups(const Shape& s) {
 
 bool use_stream(const Shape& s) { return s.T <= 64; }
 
-template <typename Elt, bool kDown>
-void launch_stream(int nt, int grid, const Args& a, hipStream_t st) {
+template <typename Elt, bool kDown, bool kStreamW>
+void launch_stream_w(int nt, int grid, const Args& a, hipStream_t st) {
     switch (nt) {
-        case 1: hipLaunchKernelGGL((k_ffn_stream<Elt, 1, kDown>), dim3(grid), dim3(256), 0, st, a); break;
-        case 2: hipLaunchKernelGGL((k_ffn_stream<Elt, 2, kDown>), dim3(grid), dim3(256), 0, st, a); break;
-        case 3: hipLaunchKernelGGL((k_ffn_stream<Elt, 3, kDown>), dim3(grid), dim3(256), 0, st, a); break;
-        default: hipLaunchKernelGGL((k_ffn_stream<Elt, 4, kDown>), dim3(grid), dim3(256), 0, st, a); break;
+        case 1: hipLaunchKernelGGL((k_ffn_stream<Elt, 1, kDown, kStreamW>), dim3(grid), dim3(256), 0, st, a); break;
+        case 2: hipLaunchKernelGGL((k_ffn_stream<Elt, 2, kDown, kStreamW>), dim3(grid), dim3(256), 0, st, a); break;
+        case 3: hipLaunchKernelGGL((k_ffn_stream<Elt, 3, kDown, kStreamW>), dim3(grid), dim3(256), 0, st, a); break;
+        default: hipLaunchKernelGGL((k_ffn_stream<Elt, 4, kDown, kStreamW>), dim3(grid), dim3(256), 0, st, a); break;
     }
+}
+
+template <typename Elt, bool kDown>
+void launch_stream(int nt, bool stream_w, int grid, const Args& a, hipStream_t st) {
+    if (stream_w) launch_stream_w<Elt, kDown, true>(nt, grid, a, st);
+    else launch_stream_w<Elt, kDown, false>(nt, grid, a, st);
+}
+
+// Non-temporal weight loads when the weights one call can touch (every slot and
+// shared expert) exceed a quarter of the 256 MB MALL: then they cannot stay in
+// the caches from one call to the next anyway.
+bool stream_weights(const Shape& s) {
+    const long long b = s.bf16 ? 2 : 4;
+    const long long bytes = 3ll * s.H * ((long long)s.slots * s.F + (long long)s.S * s.Fs) * b;
+    return bytes > (64ll << 20);
 }
 
 }  // namespace
@@ -740,6 +761,7 @@ hipError_t launch_grouped_ffn(const Shape& s, const FfnArgs& fa, hipStream_t st,
     }
     if (use_stream(s)) {
         const int nt = (s.T + 15) / 16;
+        const bool sw = stream_weights(s);
         // phase 1: 32 features per workgroup
         a.ipg_r = s.F / 32;
         a.ipg_s = s.S > 0 ? s.Fs / 32 : 1;
@@ -749,8 +771,8 @@ hipError_t launch_grouped_ffn(const Shape& s, const FfnArgs& fa, hipStream_t st,
             grid += P < 64 ? P : 64;  // pack workgroups (P >= 1 here)
         }
         if (grid > 0) {
-            if (s.bf16) launch_stream<uint16_t, false>(nt, grid, a, st);
-            else launch_stream<float, false>(nt, grid, a, st);
+            if (s.bf16) launch_stream<uint16_t, false>(nt, sw, grid, a, st);
+            else launch_stream<float, false>(nt, sw, grid, a, st);
         }
         if (hipError_t e = mark(); e != hipSuccess) return e;
         // phase 2: 64 output rows x one K chunk per workgroup
@@ -758,8 +780,8 @@ hipError_t launch_grouped_ffn(const Shape& s, const FfnArgs& fa, hipStream_t st,
         a.ipg_s = (s.H / 64) * a.ks;
         grid = a.max_routed * a.ipg_r + s.S * a.ipg_s;
         if (grid > 0) {
-            if (s.bf16) launch_stream<uint16_t, true>(nt, grid, a, st);
-            else launch_stream<float, true>(nt, grid, a, st);
+            if (s.bf16) launch_stream<uint16_t, true>(nt, sw, grid, a, st);
+            else launch_stream<float, true>(nt, sw, grid, a, st);
         }
         return hipGetLastError();
     }
