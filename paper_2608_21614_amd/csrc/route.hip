@@ -109,6 +109,8 @@ __global__ void __launch_bounds__(256)
 // id), and the wave takes the largest key and, among the lanes offering it, the
 // lowest id.  The gate of choice j is exp(s_j - s_0) / sum_j' exp(s_j' - s_0),
 // summed in j order; a score equal to the top one contributes exactly 1.
+// NS: expert slots per lane (E <= 64 NS).
+template <int NS>
 __global__ void __launch_bounds__(256)
     k_route_finish(int T, int E, int k, const float* __restrict__ part, int nsl, const float* __restrict__ bias,
                    float* __restrict__ logits, int logits_in, int32_t* __restrict__ topk_idx,
@@ -116,47 +118,46 @@ __global__ void __launch_bounds__(256)
     const int lane = lane_id();
     const int t = blockIdx.x * 4 + (threadIdx.x >> 6);
     if (t >= T) return;  // the whole wave
-    float v[4];
-    int key[4];
-    bool open[4];
-    const int nslot = (E + kWave - 1) / kWave;
+    float v[NS];
+    int key[NS];
+    bool open[NS];
 #pragma unroll
-    for (int sl = 0; sl < 4; ++sl) {
+    for (int sl = 0; sl < NS; ++sl) {
         open[sl] = lane + kWave * sl < E;
         v[sl] = 0.f;
     }
     if (logits_in) {
 #pragma unroll
-        for (int sl = 0; sl < 4; ++sl)
+        for (int sl = 0; sl < NS; ++sl)
             if (open[sl]) v[sl] = logits[(size_t)t * E + lane + kWave * sl];
     } else {
         // all slots' loads of a batch of 16 slices in flight together, bias included
-        float bv[4];
+        float bv[NS];
 #pragma unroll
-        for (int sl = 0; sl < 4; ++sl) bv[sl] = (open[sl] && bias) ? bias[lane + kWave * sl] : 0.f;
+        for (int sl = 0; sl < NS; ++sl) bv[sl] = (open[sl] && bias) ? bias[lane + kWave * sl] : 0.f;
         for (int b = 0; b < nsl; b += 16) {
-            float q[4][16];
+            float q[NS][16];
 #pragma unroll
-            for (int sl = 0; sl < 4; ++sl) {
+            for (int sl = 0; sl < NS; ++sl) {
                 const float* p = part + (size_t)t * E + (open[sl] ? lane + kWave * sl : 0);
 #pragma unroll
-                for (int j = 0; j < 16; ++j) q[sl][j] = (sl < nslot && b + j < nsl) ? p[(size_t)(b + j) * 64 * E] : 0.f;
+                for (int j = 0; j < 16; ++j) q[sl][j] = (b + j < nsl) ? p[(size_t)(b + j) * 64 * E] : 0.f;
             }
 #pragma unroll
-            for (int sl = 0; sl < 4; ++sl)
+            for (int sl = 0; sl < NS; ++sl)
 #pragma unroll
                 for (int j = 0; j < 16; ++j)
                     if (b + j < nsl) v[sl] = (b + j == 0) ? q[sl][j] : v[sl] + q[sl][j];
         }
 #pragma unroll
-        for (int sl = 0; sl < 4; ++sl)
+        for (int sl = 0; sl < NS; ++sl)
             if (open[sl]) {
                 v[sl] += bv[sl];
                 logits[(size_t)t * E + lane + kWave * sl] = v[sl];
             }
     }
 #pragma unroll
-    for (int sl = 0; sl < 4; ++sl) key[sl] = score_key(v[sl]);
+    for (int sl = 0; sl < NS; ++sl) key[sl] = score_key(v[sl]);
     float selv[8];
     int sele[8];
 #pragma unroll
@@ -166,7 +167,7 @@ __global__ void __launch_bounds__(256)
         if (j >= k) continue;  // uniform
         int kb = INT_MIN, eb = INT_MAX;
 #pragma unroll
-        for (int sl = 0; sl < 4; ++sl)
+        for (int sl = 0; sl < NS; ++sl)
             if (open[sl] && (eb == INT_MAX || key[sl] > kb)) {
                 kb = key[sl];
                 eb = lane + kWave * sl;
@@ -174,13 +175,13 @@ __global__ void __launch_bounds__(256)
         const int m = wave_max_i32(eb != INT_MAX ? kb : INT_MIN);
         const int e = wave_min_i32((eb != INT_MAX && kb == m) ? eb : INT_MAX);  // never INT_MAX: k <= E
 #pragma unroll
-        for (int sl = 0; sl < 4; ++sl)
+        for (int sl = 0; sl < NS; ++sl)
             if (lane + kWave * sl == e) open[sl] = false;
         const int es = e >> 6, el = e & 63;
         float ve = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v[0]), el));
-        if (es == 1) ve = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v[1]), el));
-        if (es == 2) ve = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v[2]), el));
-        if (es == 3) ve = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v[3]), el));
+#pragma unroll
+        for (int sl = 1; sl < NS; ++sl)
+            if (es == sl) ve = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v[sl]), el));
         selv[j] = ve;
         sele[j] = e;
     }
@@ -208,8 +209,17 @@ hipError_t launch_small(const Shape& s, const void* x, const void* w_router, con
             hipLaunchKernelGGL(k_router_partial<float>, dim3(nsl, (s.E + kScoreChunk - 1) / kScoreChunk), dim3(256), 0,
                                st, s.T, s.H, s.E, x, w_router, nsl, part);
     }
-    hipLaunchKernelGGL(k_route_finish, dim3((s.T + 3) / 4), dim3(256), 0, st, s.T, s.E, s.k, part, nsl, bias, logits,
-                       logits_in ? 1 : 0, topk_idx, topk_w);
+    const dim3 grid((s.T + 3) / 4);
+    const int li = logits_in ? 1 : 0;
+    if (s.E <= 64)
+        hipLaunchKernelGGL(k_route_finish<1>, grid, dim3(256), 0, st, s.T, s.E, s.k, part, nsl, bias, logits, li,
+                           topk_idx, topk_w);
+    else if (s.E <= 128)
+        hipLaunchKernelGGL(k_route_finish<2>, grid, dim3(256), 0, st, s.T, s.E, s.k, part, nsl, bias, logits, li,
+                           topk_idx, topk_w);
+    else
+        hipLaunchKernelGGL(k_route_finish<4>, grid, dim3(256), 0, st, s.T, s.E, s.k, part, nsl, bias, logits, li,
+                           topk_idx, topk_w);
     return hipGetLastError();
 }
 
