@@ -215,12 +215,15 @@ __device__ inline void router_scores_f32(int T, int H, int E, const float* __res
     __syncthreads();
 }
 
-// LDS ints the repack needs.
-constexpr int kRepackLdsInts = 4 * 256 + kFrontWaves * 256 + 4;
+// LDS ints the repack needs with NT threads.
+template <int NT>
+constexpr int repack_lds_ints() {
+    return 4 * 256 + (NT / 64) * 256 + 4;
+}
 
-// Expert-aligned repacking of the T*k pairs in chunks of kFrontThreads pairs
-// (chunk c = pairs [c kFrontThreads, (c + 1) kFrontThreads)); a workgroup
-// scatters the chunks [c_begin, c_end) in order:
+// Expert-aligned repacking of the T*k pairs in chunks of NT pairs (chunk c =
+// pairs [c NT, (c + 1) NT)); a workgroup of NT threads scatters the chunks
+// [c_begin, c_end) in order:
 //   1. it counts all pairs per expert, and separately the pairs before c_begin,
 //      with LDS atomics (order-free; the ids are a few tens of KB and stay in L2);
 //   2. one wave scans the counts in group order -- resident experts by id, then
@@ -235,6 +238,7 @@ constexpr int kRepackLdsInts = 4 * 256 + kFrontWaves * 256 + 4;
 //      result for any split of the chunks over workgroups.
 // The workgroup with c_begin == 0 also writes counts, seg_start and n_res.
 // ids outside [0, E) are dropped (inv_perm = -1).
+template <int NT>
 __device__ inline void repack_chunks(int T, int E, int k, int slots, int c_begin, int c_end,
                                      const int32_t* __restrict__ idx, const int32_t* __restrict__ expert_slot,
                                      int32_t* __restrict__ counts, int32_t* __restrict__ seg_start,
@@ -244,19 +248,20 @@ __device__ inline void repack_chunks(int T, int E, int k, int slots, int c_begin
     int* s_pre = lds + 256;
     int* s_base = lds + 512;
     int* s_res = lds + 768;
-    int* s_wcnt = lds + 1024;               // [16][256]
-    int* s_nres = lds + 1024 + kFrontWaves * 256;
+    constexpr int NW = NT / 64;
+    int* s_wcnt = lds + 1024;               // [NW][256]
+    int* s_nres = lds + 1024 + NW * 256;
     const int tid = threadIdx.x, wave = tid >> 6, lane = lane_id();
     const int P = T * k;
-    const int c0 = c_begin * kFrontThreads;
+    const int c0 = c_begin * NT;
 
-    for (int e = tid; e < 256; e += kFrontThreads) {
+    for (int e = tid; e < 256; e += NT) {
         s_cnt[e] = 0;
         s_pre[e] = 0;
         s_res[e] = (e < E) ? (is_resident(expert_slot[e], slots) ? 1 : 0) : 0;
     }
     __syncthreads();
-    for (int q = tid; q < P; q += kFrontThreads) {
+    for (int q = tid; q < P; q += NT) {
         const int e = idx[q];
         if (e >= 0 && e < E) {
             atomicAdd(&s_cnt[e], 1);
@@ -303,19 +308,19 @@ __device__ inline void repack_chunks(int T, int E, int k, int slots, int c_begin
     }
     __syncthreads();
     if (c_begin == 0) {
-        for (int e = tid; e < E; e += kFrontThreads) {
+        for (int e = tid; e < E; e += NT) {
             counts[e] = s_cnt[e];
             seg_start[e] = s_base[e];
         }
         if (tid == 0) *n_res = *s_nres;
     }
-    for (int e = tid; e < E; e += kFrontThreads) s_base[e] += s_pre[e];
+    for (int e = tid; e < E; e += NT) s_base[e] += s_pre[e];
 
     const unsigned long long lt_mask = (1ull << lane) - 1ull;
     for (int c = c_begin; c < c_end; ++c) {
-        for (int i = tid; i < kFrontWaves * 256; i += kFrontThreads) s_wcnt[i] = 0;
+        for (int i = tid; i < NW * 256; i += NT) s_wcnt[i] = 0;
         __syncthreads();
-        const int q = c * kFrontThreads + tid;
+        const int q = c * NT + tid;
         const int e = (q < P) ? idx[q] : -1;
         const bool valid = (e >= 0 && e < E);
         unsigned long long m = __ballot(valid);
@@ -337,10 +342,10 @@ __device__ inline void repack_chunks(int T, int E, int k, int slots, int c_begin
             inv_perm[q] = -1;
         }
         __syncthreads();
-        for (int ee = tid; ee < E; ee += kFrontThreads) {
+        for (int ee = tid; ee < E; ee += NT) {
             int sum = 0;
 #pragma unroll
-            for (int w = 0; w < kFrontWaves; ++w) sum += s_wcnt[w * 256 + ee];
+            for (int w = 0; w < NW; ++w) sum += s_wcnt[w * 256 + ee];
             s_base[ee] += sum;
         }
         __syncthreads();

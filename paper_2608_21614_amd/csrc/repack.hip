@@ -1,10 +1,11 @@
 // repack.hip -- expert-aligned token repacking with the residency split
 // (SAEM Section IV-E.1; partition by residency map, Section IV-D.2).
 //
-// A stable counting sort over the T*k pairs in chunks of 1024 (repack_chunks
-// in block_ops.hpp).  Up to kRepackGroups workgroups of 1024 threads split the
-// chunks into contiguous ranges; every workgroup counts the whole batch itself,
-// so none waits for another, and the result does not depend on the split.  A
+// A stable counting sort over the T*k pairs (repack_chunks in block_ops.hpp).
+// Up to 512 pairs (a decode batch): one workgroup of 256 threads.  Otherwise
+// chunks of 1024 pairs, split into contiguous ranges over up to kRepackGroups
+// workgroups of 1024 threads; every workgroup counts the whole batch itself, so
+// none waits for another, and the result does not depend on the split.  A
 // second small kernel packs the offloaded rows for the host.
 #include "block_ops.hpp"
 #include "kernels.hpp"
@@ -16,15 +17,16 @@ namespace {
 // (groups x T*k) and fewer cost chunk passes (chunks / groups in sequence).
 constexpr int kRepackGroups = 128;
 
-__global__ void __launch_bounds__(kFrontThreads)
+template <int NT>
+__global__ void __launch_bounds__(NT)
     k_repack(int T, int E, int k, int slots, int chunks, const int32_t* __restrict__ topk_idx,
              const int32_t* __restrict__ expert_slot, int32_t* __restrict__ counts, int32_t* __restrict__ seg_start,
              int32_t* __restrict__ perm, int32_t* __restrict__ inv_perm, int32_t* __restrict__ n_res) {
-    __shared__ int s_lds[kRepackLdsInts];
+    __shared__ int s_lds[repack_lds_ints<NT>()];
     const int g = blockIdx.x, G = gridDim.x;
     const int c_begin = (int)((long long)chunks * g / G), c_end = (int)((long long)chunks * (g + 1) / G);
-    repack_chunks(T, E, k, slots, c_begin, c_end, topk_idx, expert_slot, counts, seg_start, perm, inv_perm, n_res,
-                  s_lds);
+    repack_chunks<NT>(T, E, k, slots, c_begin, c_end, topk_idx, expert_slot, counts, seg_start, perm, inv_perm, n_res,
+                      s_lds);
 }
 
 // off_rows[p - n_res] = x[perm[p] / k]; off_w[p - n_res] = topk_w[perm[p]].
@@ -53,10 +55,16 @@ __global__ void __launch_bounds__(256)
 hipError_t launch_repack(const Shape& s, const int32_t* topk_idx, const int32_t* expert_slot, int32_t* counts,
                          int32_t* seg_start, int32_t* perm, int32_t* inv_perm, int32_t* n_res, hipStream_t st) {
     const int P = s.T * s.k;
+    if (P <= 512) {  // a decode batch: one workgroup of 256 threads, up to two chunks
+        const int chunks = (P + 255) / 256;
+        hipLaunchKernelGGL(k_repack<256>, dim3(1), dim3(256), 0, st, s.T, s.E, s.k, s.slots, chunks, topk_idx,
+                           expert_slot, counts, seg_start, perm, inv_perm, n_res);
+        return hipGetLastError();
+    }
     const int chunks = (P + kFrontThreads - 1) / kFrontThreads;
-    const int groups = chunks < 1 ? 1 : (chunks < kRepackGroups ? chunks : kRepackGroups);
-    hipLaunchKernelGGL(k_repack, dim3((unsigned)groups), dim3(kFrontThreads), 0, st, s.T, s.E, s.k, s.slots, chunks,
-                       topk_idx, expert_slot, counts, seg_start, perm, inv_perm, n_res);
+    const int groups = chunks < kRepackGroups ? chunks : kRepackGroups;
+    hipLaunchKernelGGL(k_repack<kFrontThreads>, dim3((unsigned)groups), dim3(kFrontThreads), 0, st, s.T, s.E, s.k,
+                       s.slots, chunks, topk_idx, expert_slot, counts, seg_start, perm, inv_perm, n_res);
     return hipGetLastError();
 }
 
