@@ -171,6 +171,10 @@ __device__ __forceinline__ int group_token(const Args& a, const Group& g, int n)
 // stream kernel (decode)
 // ---------------------------------------------------------------------------
 
+// 16-row weight tiles per stream workgroup: two with a single token tile (twice
+// the workgroups, for the small grids of the smallest batches), else four.
+constexpr int stream_mt(int nt) { return nt == 1 ? 2 : 4; }
+
 // kStreamW: the weights are loaded non-temporally (they do not stay in the
 // caches for a later use), which raises the streaming rate when the call's
 // weights are far larger than the caches; small weight sets that stay in the
@@ -178,7 +182,8 @@ __device__ __forceinline__ int group_token(const Args& a, const Group& g, int n)
 template <typename Elt, int NT, bool kDown, bool kStreamW>
 __global__ void __launch_bounds__(256) k_ffn_stream(Args a) {
     using F8 = Frag8<Elt>;
-    constexpr int MT = 4;                          // 16-row weight tiles per workgroup
+    constexpr int MT = stream_mt(NT);              // 16-row weight tiles per workgroup
+    constexpr int MH = MT / 2;                     // phase 1: gate tiles (then as many up tiles)
     constexpr int U = sizeof(Elt) == 2 ? 2 : 1;    // K steps per load batch (two batches in flight)
     __shared__ int s_list[256];
     __shared__ int s_wsum[4];
@@ -216,19 +221,19 @@ __global__ void __launch_bounds__(256) k_ffn_stream(Args a) {
     const Elt* wp[MT];
     int row0, kc = 0, c0, c1;
     if (!kDown) {
-        const int f0 = sub * 32;
+        const int f0 = sub * 16 * MH;
         row0 = f0;
         const int nst = a.H / 32;
         const Elt* w = reinterpret_cast<const Elt*>(g.w13);
 #pragma unroll
         for (int m = 0; m < MT; ++m) {
-            const int rt = (m < 2 ? 0 : g.Fg / 16) + f0 / 16 + (m & 1);  // gate tiles, then up tiles
+            const int rt = (m < MH ? 0 : g.Fg / 16) + f0 / 16 + m % MH;  // gate tiles, then up tiles
             wp[m] = w + (size_t)rt * nst * 512 + lane * 8;
         }
         c0 = 0;
         c1 = nst;
     } else {
-        const int h0 = (sub / a.ks) * 64;
+        const int h0 = (sub / a.ks) * 16 * MT;
         kc = sub % a.ks;
         row0 = h0;
         const int nst = g.Fg / 32;
@@ -329,18 +334,18 @@ __global__ void __launch_bounds__(256) k_ffn_stream(Args a) {
     __syncthreads();
 
     if (!kDown) {
-        // pair gate tile m with up tile m + 2; lane l holds features 4*(l/16)..+3 of token l%16
-        for (int task = threadIdx.x; task < 2 * NT * kWave; task += 256) {
+        // pair gate tile m with up tile m + MH; lane l holds features 4*(l/16)..+3 of token l%16
+        for (int task = threadIdx.x; task < MH * NT * kWave; task += 256) {
             const int m = task / (NT * kWave);
             const int j = (task / kWave) % NT;
             const int l = task % kWave;
             const int n = 16 * j + (l & 15);
             if (j >= ntile || n >= g.count) continue;
-            f32x4 gv = s_red[0][m][j][l], uv = s_red[0][m + 2][j][l];
+            f32x4 gv = s_red[0][m][j][l], uv = s_red[0][m + MH][j][l];
 #pragma unroll
             for (int w = 1; w < 4; ++w) {
                 gv += s_red[w][m][j][l];
-                uv += s_red[w][m + 2][j][l];
+                uv += s_red[w][m + MH][j][l];
             }
             const int f = row0 + 16 * m + 4 * (l >> 4);
             const f32x4 av = {silu(gv.x) * uv.x, silu(gv.y) * uv.y, silu(gv.z) * uv.z, silu(gv.w) * uv.w};
@@ -711,8 +716,8 @@ bool ffn_packs_offloaded(const Shape& s) { return use_stream(s); }
 
 int ffn_down_splits(const Shape& s) {
     if (!use_stream(s)) return 1;
-    // Phase-2 work items: (groups) x (H / 64 row tiles) x ks, each streaming 64
-    // rows of one K chunk.  Smallest ks (a power of two <= 16) such that
+    // Phase-2 work items: (groups) x (H / rows) x ks, each streaming `rows` rows
+    // (16 per weight tile) of one K chunk.  Smallest ks (a power of two <= 16) such that
     //  * there are >= 512 workgroups (two per CU), and
     //  * the longest workgroup streams at most 1/400 of the phase's weights: one
     //    workgroup streams at about 1/200 of the chip's HBM rate, so with a 2x
@@ -726,7 +731,8 @@ int ffn_down_splits(const Shape& s) {
     if (s.S > 0 && s.Fs / 32 < steps) steps = s.Fs / 32;
     const long long kmax = (s.S > 0 && s.Fs > s.F) ? s.Fs : s.F;
     const long long weights = (groups_r * s.F + (long long)s.S * s.Fs) * s.H;  // elements, worst case
-    auto balanced = [&](int ks) { return groups * (s.H / 64) * ks >= 512 && 64 * kmax / ks * 400 <= weights; };
+    const long long rows = 16 * stream_mt((s.T + 15) / 16);
+    auto balanced = [&](int ks) { return groups * (s.H / rows) * ks >= 512 && rows * kmax / ks * 400 <= weights; };
     int ks = 1;
     while (ks < 16 && !balanced(ks) && steps / (ks * 2) >= 16) ks *= 2;
     return ks;
@@ -763,8 +769,9 @@ hipError_t launch_grouped_ffn(const Shape& s, const FfnArgs& fa, hipStream_t st,
         const int nt = (s.T + 15) / 16;
         const bool sw = stream_weights(s);
         // phase 1: 32 features per workgroup
-        a.ipg_r = s.F / 32;
-        a.ipg_s = s.S > 0 ? s.Fs / 32 : 1;
+        const int mt = stream_mt(nt);
+        a.ipg_r = s.F / (8 * mt);
+        a.ipg_s = s.S > 0 ? s.Fs / (8 * mt) : 1;
         int grid = a.max_routed * a.ipg_r + s.S * a.ipg_s;
         if (fa.off_rows || fa.off_w) {
             const int P = s.T * s.k;
@@ -776,8 +783,8 @@ hipError_t launch_grouped_ffn(const Shape& s, const FfnArgs& fa, hipStream_t st,
         }
         if (hipError_t e = mark(); e != hipSuccess) return e;
         // phase 2: 64 output rows x one K chunk per workgroup
-        a.ipg_r = (s.H / 64) * a.ks;
-        a.ipg_s = (s.H / 64) * a.ks;
+        a.ipg_r = (s.H / (16 * mt)) * a.ks;
+        a.ipg_s = (s.H / (16 * mt)) * a.ks;
         grid = a.max_routed * a.ipg_r + s.S * a.ipg_s;
         if (grid > 0) {
             if (s.bf16) launch_stream<uint16_t, true>(nt, sw, grid, a, st);
