@@ -46,3 +46,26 @@ def test_random_shape(moe, i):
     lay = make_layer(T, H, E, F, k, dtype=dtype, shared=S, shared_ffn=Fs, n_resident=res, residency="random",
                      bias="zipf", seed=77 + i)
     run_and_check_layer(moe, lay)
+
+
+@pytest.mark.parametrize("i", range(12))
+def test_random_shape_hybrid(moe, i):
+    """The hybrid layer (offloaded experts on the host, merged by the combine) on random shapes with
+    offloaded experts: the full output against the oracle's resident + offloaded sum."""
+    from test_gpu_hybrid import run_hybrid
+    from gpu_support import TOL
+    rng = np.random.default_rng(3000 + i)
+    T = int(rng.choice([1, 5, 16, 33, 64, 80]))
+    H = int(rng.choice([64, 128, 256]))
+    E = int(rng.choice([4, 8, 20, 64]))
+    k = int(rng.integers(1, min(E, 8) + 1))
+    F = int(rng.choice([64, 128, 320]))
+    S = int(rng.choice([0, 1]))
+    Fs = 128 if S else 0
+    dtype = "f32" if i % 4 == 3 else "bf16"
+    res = int(rng.integers(0, E))                       # at least one expert offloaded
+    print(f"[case] hybrid sweep {i}: T={T} H={H} E={E} F={F} k={k} S={S} {dtype} resident={res}", flush=True)
+    lay = make_layer(T, H, E, F, k, dtype=dtype, shared=S, shared_ffn=Fs, n_resident=res, residency="random",
+                     bias="zipf", seed=500 + i)
+    err, n_res, _ = run_hybrid(lay, threads=4)
+    assert err <= TOL[dtype]
