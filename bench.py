@@ -437,6 +437,13 @@ def main() -> int:
         "ms_per_step_without_events": ms_no_events,
         "hbm_read_probe_GBps": read_probe_gbps,
         "mfma_tflops_layer_algorithmic": alg["flops"] / (ms_per_step * 1e-3) / 1e12,
+        # whole layer against its roofline: the slower of moving its algorithmic bytes at
+        # the HBM peak and doing its algorithmic flops at the dense bf16 MFMA peak
+        "layer_roofline": {
+            "t_roof_us": max(alg["layer_bytes"] / (HBM_PEAK_GBPS * 1e9), alg["flops"] / (MFMA_BF16_PEAK_TFLOPS * 1e12)) * 1e6,
+            "bound": "hbm" if alg["layer_bytes"] / HBM_PEAK_GBPS > alg["flops"] / MFMA_BF16_PEAK_TFLOPS * 1e3 else "mfma",
+            "frac": max(alg["layer_bytes"] / (HBM_PEAK_GBPS * 1e9), alg["flops"] / (MFMA_BF16_PEAK_TFLOPS * 1e12))
+            / (ms_per_step * 1e-3)},
         "roofline": roofline,
     }
     if args.bookkeeping > 0:
