@@ -86,6 +86,16 @@ def algorithmic_bytes(cfg, counts, resident):
                 layer_bytes=layer, flops=flops, phase1_flops=4 * H * F * n_res + cfg.shared * 4 * H * cfg.shared_ffn * T)
 
 
+def layer_roofline(alg, ms_per_step: float):
+    """The whole layer against its roofline: the slower of moving its algorithmic bytes at the HBM
+    peak and doing its algorithmic flops at the dense bf16 MFMA peak."""
+    t_bytes = alg["layer_bytes"] / (HBM_PEAK_GBPS * 1e9)
+    t_flops = alg["flops"] / (MFMA_BF16_PEAK_TFLOPS * 1e12)
+    t_roof = max(t_bytes, t_flops)
+    return {"t_roof_us": t_roof * 1e6, "t_bytes_us": t_bytes * 1e6, "t_flops_us": t_flops * 1e6,
+            "bound": "hbm" if t_bytes >= t_flops else "mfma", "frac": t_roof / (ms_per_step * 1e-3)}
+
+
 def cpu_baseline(layer, seconds: float):
     """The CPU oracle (as it stands) on the same layer: whole batches until `seconds` have passed."""
     import oracle
@@ -439,11 +449,7 @@ def main() -> int:
         "mfma_tflops_layer_algorithmic": alg["flops"] / (ms_per_step * 1e-3) / 1e12,
         # whole layer against its roofline: the slower of moving its algorithmic bytes at
         # the HBM peak and doing its algorithmic flops at the dense bf16 MFMA peak
-        "layer_roofline": {
-            "t_roof_us": max(alg["layer_bytes"] / (HBM_PEAK_GBPS * 1e9), alg["flops"] / (MFMA_BF16_PEAK_TFLOPS * 1e12)) * 1e6,
-            "bound": "hbm" if alg["layer_bytes"] / HBM_PEAK_GBPS > alg["flops"] / MFMA_BF16_PEAK_TFLOPS * 1e3 else "mfma",
-            "frac": max(alg["layer_bytes"] / (HBM_PEAK_GBPS * 1e9), alg["flops"] / (MFMA_BF16_PEAK_TFLOPS * 1e12))
-            / (ms_per_step * 1e-3)},
+        "layer_roofline": layer_roofline(alg, ms_per_step),
         "roofline": roofline,
     }
     if args.bookkeeping > 0:
