@@ -74,9 +74,9 @@ def test_committed_traffic_matches_the_current_kernels(workload):
 
 
 def test_layer_roofline_bound_and_fraction():
-    alg = {"layer_bytes": 8e9 * 100e-6, "flops": 2.5e15 * 40e-6}      # 100 us of bytes, 40 us of flops
+    alg = {"layer_bytes": 8e12 * 100e-6, "flops": 2.5e15 * 40e-6}     # 100 us of bytes, 40 us of flops
     r = bench.layer_roofline(alg, ms_per_step=0.2)
     assert r["bound"] == "hbm" and abs(r["t_roof_us"] - 100.0) < 1e-9 and abs(r["frac"] - 0.5) < 1e-12
-    alg = {"layer_bytes": 8e9 * 10e-6, "flops": 2.5e15 * 50e-6}
+    alg = {"layer_bytes": 8e12 * 10e-6, "flops": 2.5e15 * 50e-6}
     r = bench.layer_roofline(alg, ms_per_step=0.1)
     assert r["bound"] == "mfma" and abs(r["t_roof_us"] - 50.0) < 1e-9 and abs(r["frac"] - 0.5) < 1e-12
