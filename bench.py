@@ -208,11 +208,13 @@ def bookkeeping_timings(dev, n: int):
             "timing": "wall clock per call, device synchronised before and after each call"}
 
 
-def trace_timings(seed: int, lags):
+def trace_timings(seed: int, lags, detect: bool = False):
     """The stage-structured decode trace with real slot copies (Section IV-C), per prefetch lag.
 
     Routers, stage biases and per-call activations are the trace's own (so the
-    residency trajectory and CHR are the ones the parity tests check); every
+    residency trajectory and CHR are the ones the parity tests check).  With
+    `detect`, the boundaries come from the cue machine on the batch's generated
+    tokens (Section IV-B.1) instead of the trace's true stage ends.  Every
     (layer, expert) gets its own pinned host buffer filled with one seeded
     expert's weights -- the values do not change routing, copies or kernel time.
     """
@@ -232,6 +234,12 @@ def trace_timings(seed: int, lags):
     base13, base2 = layers[0].w13(0), layers[0].w2(0)
     out = {"steps": c.steps, "layers": L, "stages": int(trace.n_stages), "batch": c.batch, "slots": c.n_slots,
            "weights": "one seeded expert's weights in every (layer, expert) host buffer", "runs": []}
+    detector = None
+    if detect:
+        ts = trace.token_stream()
+        detector = {"cues": ts["cues"], "stream": ts["stream"]}
+        out["boundaries"] = "detected from cues in the generated tokens"
+        out["planted_boundaries"] = int(len(ts["planted"]))
     runner = None
     for lag in lags:
         log(f"[bench] trace run, prefetch lag {lag}")
@@ -241,12 +249,12 @@ def trace_timings(seed: int, lags):
             runner.prepare_host_weights()
         else:   # same host buffers and slot pools, fresh trajectory
             runner.reset(lag)
-        r = runner.run()
+        r = runner.run(detector=detector)
         calls = r["calls"]
         out["runs"].append({"lag": lag, "trace_ms": r["trace_ms"], "us_per_layer_call": r["trace_ms"] * 1e3 / calls,
                             "chr_online": r["chr_online"], "copied_experts": r["copied_experts"],
                             "copy_ms_total": r["copy_ms_total"], "copy_GBps": r["copy_GBps"],
-                            "stall_ms_total": r["stall_ms_total"]})
+                            "stall_ms_total": r["stall_ms_total"], "boundaries": int(len(r["boundary_steps"]))})
         log(f"[bench]   {out['runs'][-1]}")
     return out
 
@@ -273,6 +281,9 @@ def main() -> int:
     ap.add_argument("--trace", type=str, default="", metavar="LAGS",
                     help="with --workload c5_stage_trace: also run the whole stage-structured trace with real "
                          "slot copies, once per comma-separated prefetch lag (e.g. 0,8); extra object")
+    ap.add_argument("--detect", action="store_true",
+                    help="with --trace: stage boundaries from the cue machine on the generated tokens "
+                         "(Section IV-B.1) instead of the trace's true stage ends")
     ap.add_argument("--calib-copy-mib", type=int, default=0,
                     help="run one plain device copy of this many MiB first (counter calibration)")
     args = ap.parse_args()
@@ -462,7 +473,7 @@ def main() -> int:
     if args.trace:
         del copies, dev
         torch.cuda.empty_cache()
-        result["trace"] = trace_timings(args.seed, [int(v) for v in args.trace.split(",")])
+        result["trace"] = trace_timings(args.seed, [int(v) for v in args.trace.split(",")], args.detect)
     if not args.no_cpu_baseline:
         log("[bench] timing the CPU oracle")
         result["cpu_baseline"] = cpu_baseline(layer, args.cpu_seconds)

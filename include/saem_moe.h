@@ -311,6 +311,41 @@ moe_status moe_offload_plan(int32_t experts, const int32_t* counts, const int32_
                             const moe_offload_rates* rates, int32_t max_copies, int32_t* choice);
 
 /*
+ * Stage-boundary detection (Section IV-B.1, sliding-window pattern matching):
+ * a finite-state machine over generated token ids recognises transition cues
+ * (each a sequence of one or more token ids: a cue word split into subword
+ * tokens) in every sequence of a batch, fed one token per sequence per decode
+ * step.  Partial matches carry across steps, so a multi-token cue is reported
+ * the step its last token arrives.  A match in any sequence is a stage
+ * transition for the batch (Section IV-B.2 aggregates over all queries).
+ * Host memory only; no device work.
+ *
+ * moe_cue_fsm_words: int32 words the machine needs for cues of `total_tokens`
+ * tokens in all (5 * total_tokens + 8); -1 if total_tokens < 0.
+ *
+ * moe_cue_build: builds the machine into fsm [fsm_words] (caller-owned).
+ *   cue_offsets [n_cues + 1]: cue c is cue_tokens[cue_offsets[c] .. cue_offsets[c+1]);
+ *   cue_offsets[0] = 0, every cue has at least one token, token ids >= 0.
+ *   n_cues = 0 builds a machine that never matches (offsets and tokens may be NULL).
+ *   Identical cues are allowed; a match reports the lowest of their ids.
+ *   Errors: MOE_ERR_INVALID_ARG for malformed cues, MOE_ERR_WORKSPACE if
+ *   fsm_words < moe_cue_fsm_words(total); nothing is written then.
+ *
+ * moe_cue_step: advances `batch` sequences by one token each.
+ *   tokens [batch]: the token each sequence generated this step; a negative id
+ *   means none (the sequence is idle or finished): its window restarts.
+ *   state [batch] in/out: 0 for a fresh sequence, else the value the previous
+ *   call left.  matched [batch] out: id of the longest cue that ends with this
+ *   token, or -1.  MOE_ERR_INVALID_ARG (nothing written) for a machine not made by
+ *   moe_cue_build or a state out of range.
+ */
+int64_t moe_cue_fsm_words(int64_t total_tokens);
+moe_status moe_cue_build(int32_t n_cues, const int32_t* cue_offsets, const int32_t* cue_tokens, int32_t* fsm,
+                         int64_t fsm_words);
+moe_status moe_cue_step(const int32_t* fsm, int32_t batch, const int32_t* tokens, int32_t* state,
+                        int32_t* matched);
+
+/*
  * Measurement utility (not a step of the method): reads `bytes` of device
  * memory at src once, with 16-byte loads spread over the whole GPU, so that the
  * caller can time the streaming-read rate of this GPU's HBM on its stream and

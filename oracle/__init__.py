@@ -396,3 +396,64 @@ def stage_replay(counts: np.ndarray, stage_len: np.ndarray, initial_slot: np.nda
     chr_cv = hit_cv / total if total else 1.0
     return {"slot_history": hist, "resident": resident, "chr_online": chr_on, "chr_clairvoyant": chr_cv,
             "eta_chr": chr_on / chr_cv if chr_cv else 1.0}
+
+
+# --------------------------------------------------------------------------
+# Stage-boundary detection (Section IV-B.1)
+# --------------------------------------------------------------------------
+
+def cue_matches(cues: Sequence[Sequence[int]], stream: np.ndarray) -> np.ndarray:
+    """Transition-cue matches in generated token streams (Section IV-B.1).
+
+    stream[step, b] is the token that sequence b generated at decode step
+    `step`; a negative id means no token, and the sequence's window restarts
+    there.  After every step the detector checks whether the window of recent
+    tokens of each sequence ends with one of the cues (a cue being one or more
+    token ids).  Written as that definition: every cue is compared with the
+    tail of every window.  Returns [steps, B] int32: the id of the longest cue
+    equal to the window's tail after the step (identical cues: the lowest id),
+    or -1 when none is.
+    """
+    s = np.asarray(stream, dtype=np.int64)
+    if s.ndim == 1:
+        s = s[:, None]
+    steps, B = s.shape
+    # tokens in the window after each step (since the last restart)
+    window = np.zeros((steps, B), dtype=np.int64)
+    run = np.zeros(B, dtype=np.int64)
+    for i in range(steps):
+        run = np.where(s[i] < 0, 0, run + 1)
+        window[i] = run
+    best = np.full((steps, B), -1, dtype=np.int32)
+    best_len = np.zeros((steps, B), dtype=np.int64)
+    for cid, cue in enumerate(cues):
+        c = [int(t) for t in cue]
+        L = len(c)
+        if L == 0:
+            continue
+        hit = window >= L
+        for j in range(L):           # token j of the cue sits L-1-j steps back
+            back = L - 1 - j
+            shifted = np.full((steps, B), -2, dtype=np.int64)
+            shifted[back:] = s[:steps - back]
+            hit &= shifted == c[j]
+        take = hit & (L > best_len)  # longer wins; equal length keeps the earlier (lower) id
+        best[take] = cid
+        best_len[take] = L
+    return best
+
+
+def stage_lengths_from_events(matched: np.ndarray, steps: int) -> np.ndarray:
+    """Stages delimited by detected transitions (Section IV-B.2: one timeline for the batch).
+
+    A cue matched in any sequence at step i ends the current stage with that
+    step; the next stage starts at i + 1.  A match at the last step starts no
+    stage.  Returns the stage lengths, summing to `steps`.
+    """
+    m = np.asarray(matched)
+    if m.ndim == 1:
+        m = m[:, None]
+    ev = np.flatnonzero((m[:steps] >= 0).any(axis=1))
+    cuts = [int(i) + 1 for i in ev if int(i) + 1 < steps]
+    edges = [0] + cuts + [steps]
+    return np.diff(np.asarray(edges, dtype=np.int64))

@@ -27,6 +27,7 @@ EXPORTED = [
     "moe_abi_version", "moe_status_str", "moe_check_dims", "moe_workspace_bytes", "moe_route_topk",
     "moe_repack", "moe_grouped_ffn", "moe_combine", "moe_layer_forward", "moe_stage_accumulate",
     "moe_stage_plan", "moe_pack_weights", "moe_host_ffn", "moe_offload_plan", "moe_read_probe",
+    "moe_cue_fsm_words", "moe_cue_build", "moe_cue_step",
 ]
 
 
@@ -109,6 +110,9 @@ def _load() -> ctypes.CDLL:
                          ctypes.c_int),
         "moe_offload_plan": ([i32, _vp, _vp, i32, ctypes.POINTER(moe_offload_rates), i32, _vp], ctypes.c_int),
         "moe_read_probe": ([_vp, ctypes.c_int64, _vp, _vp], ctypes.c_int),
+        "moe_cue_fsm_words": ([ctypes.c_int64], ctypes.c_int64),
+        "moe_cue_build": ([i32, _vp, _vp, _vp, ctypes.c_int64], ctypes.c_int),
+        "moe_cue_step": ([_vp, i32, _vp, _vp, _vp], ctypes.c_int),
     }
     for name, (args, res) in sig.items():
         fn = getattr(lib, name)
@@ -279,3 +283,29 @@ def moe_stage_plan(log_host, prev_slot_host, slots: int):
     _check(lib.moe_stage_plan(int(log.size), int(slots), log.ctypes.data, prev.ctypes.data, new.ctypes.data),
            "moe_stage_plan")
     return new
+
+
+def moe_cue_build(cues):
+    """Stage-boundary cue machine (Section IV-B.1) from a list of token-id sequences -> numpy int32 words."""
+    import numpy as np
+    seqs = [np.asarray(c, dtype=np.int64).ravel() for c in cues]
+    off = np.zeros(len(seqs) + 1, dtype=np.int32)
+    if seqs:
+        off[1:] = np.cumsum([len(c) for c in seqs])
+    toks = (np.concatenate(seqs) if seqs else np.zeros(0)).astype(np.int32)
+    words = int(lib.moe_cue_fsm_words(int(off[-1])))
+    fsm = np.zeros(max(words, 1), dtype=np.int32)
+    _check(lib.moe_cue_build(len(seqs), off.ctypes.data, toks.ctypes.data, fsm.ctypes.data, words), "moe_cue_build")
+    return fsm
+
+
+def moe_cue_step(fsm, tokens, state):
+    """Feeds one token per sequence (numpy int32 [B]); updates `state` in place -> matched cue ids [B] (-1: none)."""
+    import numpy as np
+    tok = np.ascontiguousarray(tokens, dtype=np.int32)
+    if state.dtype != np.int32 or not state.flags.c_contiguous or state.shape != tok.shape:
+        raise ValueError("state must be a C-contiguous int32 array shaped like tokens")
+    matched = np.empty_like(tok)
+    _check(lib.moe_cue_step(fsm.ctypes.data, int(tok.size), tok.ctypes.data, state.ctypes.data, matched.ctypes.data),
+           "moe_cue_step")
+    return matched

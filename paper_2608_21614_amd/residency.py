@@ -30,8 +30,8 @@ from typing import Callable, Dict, List, Optional
 import numpy as np
 import torch
 
-from . import (MOE_BF16, MOE_F32, layer_args, make_dims, moe_layer_forward, moe_pack_weights, moe_stage_accumulate,
-               moe_stage_plan, moe_workspace_bytes)
+from . import (MOE_BF16, MOE_F32, layer_args, make_dims, moe_cue_build, moe_cue_step, moe_layer_forward,
+               moe_pack_weights, moe_stage_accumulate, moe_stage_plan, moe_workspace_bytes)
 from .device import to_device, to_host
 
 
@@ -112,14 +112,28 @@ class StageResidencyRunner:
             moe_pack_weights(self.st2, self.w2[l][s], stream=stream)
 
     # -- trace ------------------------------------------------------------------
-    def run(self, steps: Optional[int] = None, keep_outputs=(), log_every: int = 0) -> dict:
-        """Runs the first `steps` steps.  keep_outputs: (step, layer) pairs whose outputs are kept."""
+    def run(self, steps: Optional[int] = None, keep_outputs=(), log_every: int = 0,
+            detector: Optional[dict] = None) -> dict:
+        """Runs the first `steps` steps.  keep_outputs: (step, layer) pairs whose outputs are kept.
+
+        Stage boundaries: without a detector, the trace's own stage ends.  With
+        ``detector = {"cues": [...], "stream": [steps, batch] int32}`` they come
+        from the cue machine (Section IV-B.1): after every step the batch's
+        generated tokens are fed to ``moe_cue_step``, and a cue matched in any
+        sequence ends the stage with that step (false positives included).  The
+        router bias still follows the trace's true stages.
+        """
         c, tr = self.cfg, self.trace
         L, E, T, k = c.layers, c.experts, c.batch, c.top_k
         steps = c.steps if steps is None else int(steps)
         main = torch.cuda.current_stream(self.device)
         stage_of = tr.stage_of_step()
-        ends = set(int(v) for v in tr.stage_ends())
+        ends = set(int(v) for v in tr.stage_ends()[:-1])
+        if detector is not None:
+            fsm = moe_cue_build(detector["cues"])
+            tokens = np.ascontiguousarray(detector["stream"], dtype=np.int32)
+            cue_state = np.zeros(tokens.shape[1], dtype=np.int32)
+        boundary_steps = []
         counts = torch.empty((steps, L, E), dtype=torch.int32, device=self.device)
         n_res = torch.empty((steps, L), dtype=torch.int32, device=self.device)
         kept = {}
@@ -169,7 +183,12 @@ class StageResidencyRunner:
                 if (step, l) in keep:
                     kept[(step, l)] = out
             used_slot[step] = cur
-            if step in ends and s + 1 < tr.n_stages:
+            if detector is not None:
+                boundary = bool((moe_cue_step(fsm, tokens[step], cue_state) >= 0).any())
+            else:
+                boundary = step in ends
+            if boundary and step + 1 < steps:
+                boundary_steps.append(step)
                 if pending is not None:   # a stage shorter than the lag: its copies must land first
                     finish_pending()
                 h_log = to_host(self.log)                        # waits for this stage's calls
@@ -222,4 +241,5 @@ class StageResidencyRunner:
             "copy_GBps": (n_copied * expert_bytes / (sum(copy_ms) * 1e-3) / 1e9) if copy_ms else None,
             "stall_ms_total": float(sum(a.elapsed_time(b_) for a, b_ in stalls)),
             "boundaries_with_copies": len(self.copies), "lag": self.lag,
+            "boundary_steps": np.asarray(boundary_steps, dtype=np.int64),
         }

@@ -11,6 +11,12 @@ test, since routing does not depend on residency):
 * the resident pairs of every call and the online CHR;
 * every slot's bytes == the packed weights of the expert the plan put there;
 * the layer output of sampled calls == the oracle's resident partial sum.
+
+With ``detect``, the boundaries come from the cue machine fed the batch's
+generated tokens after every step (Section IV-B.1), on a token stream with a
+small vocabulary so that background text also completes cues: the runner's
+boundaries must be the oracle's cue events, and the replay runs over the stages
+those events delimit, not the trace's true ones.
 """
 from __future__ import annotations
 
@@ -33,12 +39,12 @@ def say(*a):
     print("[residency]", *a, flush=True)
 
 
-@pytest.mark.parametrize("lag", [0, 3])
-def test_stage_residency_with_slot_copies(lag):
+@pytest.mark.parametrize("lag,detect", [(0, False), (3, False), (2, True)])
+def test_stage_residency_with_slot_copies(lag, detect):
     import paper_2608_21614_amd as moe
     from paper_2608_21614_amd.device import to_device
     from paper_2608_21614_amd.residency import StageResidencyRunner
-    c = SMALL
+    c = replace(SMALL, vocab=200, cue_min_rank=10) if detect else SMALL
     trace = StageTrace(c, seed=1)
     L, E, T, k, H = c.layers, c.experts, c.batch, c.top_k, c.hidden
     layers = [trace.layer(l) for l in range(L)]
@@ -47,7 +53,16 @@ def test_stage_residency_with_slot_copies(lag):
     sample = [(0, 0), (int(ends[0]) + 1, 1), (min(int(ends[1]) + 2, c.steps - 1), 0), (c.steps - 1, 1)]
     run = StageResidencyRunner(trace, [lay.w_router for lay in layers],
                                lambda l, e: (layers[l].w13(e), layers[l].w2(e)), trace.x, lag=lag)
-    r = run.run(keep_outputs=sample)
+    detector, stage_len = None, trace.stage_len
+    if detect:
+        ts = trace.token_stream()
+        detector = {"cues": ts["cues"], "stream": ts["stream"]}
+        matched = oracle.cue_matches(ts["cues"], ts["stream"])
+        stage_len = oracle.stage_lengths_from_events(matched, c.steps)
+        say(f"detected stages {stage_len.tolist()} (true {trace.stage_len.tolist()})")
+        assert len(stage_len) > trace.n_stages            # false positives split true stages
+    r = run.run(keep_outputs=sample, detector=detector)
+    np.testing.assert_array_equal(r["boundary_steps"], np.cumsum(stage_len)[:-1] - 1)
     say(f"CHR {r['chr_online']:.4f}, {r['copied_experts']} experts copied at {r['boundaries_with_copies']} "
         f"boundaries, stall {r['stall_ms_total']:.3f} ms")
     assert r["copied_experts"] > 0
@@ -56,7 +71,7 @@ def test_stage_residency_with_slot_copies(lag):
     for l in range(L):
         ids = np.flatnonzero(trace.initial_resident[l])
         init[l, ids] = np.arange(len(ids))
-    ref = oracle.stage_replay(r["counts"], trace.stage_len, init, c.n_slots, lag=lag)
+    ref = oracle.stage_replay(r["counts"], stage_len, init, c.n_slots, lag=lag)
     np.testing.assert_array_equal(r["slot_history"], ref["slot_history"])
     np.testing.assert_array_equal(r["used_slot"] >= 0, ref["resident"])
     np.testing.assert_array_equal(r["n_res"], (r["counts"] * ref["resident"]).sum(axis=2))

@@ -45,6 +45,7 @@ __all__ = [
 # tags of the per-tensor random streams
 _TAG_X, _TAG_WR, _TAG_W13, _TAG_W2, _TAG_WS13, _TAG_WS2 = 1, 2, 3, 4, 5, 6
 _TAG_BIAS, _TAG_RES, _TAG_SLOT, _TAG_STAGE, _TAG_DIR = 7, 8, 9, 10, 11
+_TAG_CUE, _TAG_TOK, _TAG_PLANT = 12, 13, 14
 
 _CHUNK = 1 << 22  # elements per independent stream chunk
 _THREADS = max(1, min(16, int(os.environ.get("MOE_GEN_THREADS", os.cpu_count() or 1))))
@@ -163,6 +164,12 @@ class TraceConfig:
     x_std: float = 1.0
     w_std: float = 0.02
     dtype: str = "bf16"
+    # generated-token stream of the batch with transition cues at the stage boundaries
+    vocab: int = 32000
+    n_cues: int = 12
+    max_cue_len: int = 4
+    token_zipf_s: float = 1.1
+    cue_min_rank: int = 1000        # cue tokens are drawn from popularity ranks >= this
 
     def layer_config(self) -> MoEConfig:
         return MoEConfig(self.name, self.dtype, tokens=self.batch, hidden=self.hidden,
@@ -348,6 +355,62 @@ class StageTrace:
     def x(self, step: int, layer: int) -> np.ndarray:
         c = self.cfg
         return _normal(self.seed, (layer, _TAG_X, 1 + step), (c.batch, c.hidden), c.x_std, c.dtype)
+
+    def cues(self) -> list:
+        """Synthetic transition cues: n_cues token-id sequences of 1..max_cue_len tokens.
+
+        They stand in for a model's cue phrases ("Alternatively", "On second
+        thought", ...) split into subword tokens; the first cue has one token so
+        that every boundary can take a cue.  Tokens come from the less popular
+        part of the vocabulary (ranks >= cue_min_rank of the background's Zipf
+        order), so background text completes a cue only now and then.
+        """
+        c = self.cfg
+        rng = _rng(self.seed, 0, _TAG_CUE, 0)
+        order = self._token_order()
+        out = []
+        for i in range(c.n_cues):
+            n = 1 if i == 0 else int(rng.integers(1, c.max_cue_len + 1))
+            ranks = rng.integers(c.cue_min_rank, c.vocab, size=n)
+            out.append([int(order[r]) for r in ranks])
+        return out
+
+    def _token_order(self) -> np.ndarray:
+        """Token id of each popularity rank (a seeded permutation of the vocabulary)."""
+        return _rng(self.seed, 0, _TAG_TOK, 0).permutation(self.cfg.vocab)
+
+    def token_stream(self) -> dict:
+        """Generated tokens of the batch, [steps, batch] int32, with the cues planted at the boundaries.
+
+        Background tokens are Zipf(token_zipf_s) over the vocabulary.  For every
+        stage after the first, one sequence (seeded, never the one of the
+        previous boundary) generates a cue whose last token falls on the last
+        step of the previous stage, so a detector that matches cues sees the
+        transition exactly at the planted boundary.  Returns stream, cues and
+        planted (the step of each planted cue's last token).
+        """
+        c = self.cfg
+        steps, B = c.steps, c.batch
+        order = self._token_order()
+        p = np.arange(1, c.vocab + 1, dtype=np.float64) ** (-c.token_zipf_s)
+        p /= p.sum()
+        ranks = _rng(self.seed, 0, _TAG_TOK, 1).choice(c.vocab, size=(steps, B), p=p)
+        stream = order[ranks].astype(np.int32)
+        cues = self.cues()
+        rng = _rng(self.seed, 0, _TAG_PLANT, 0)
+        planted = []
+        prev_b = -1
+        for a in np.cumsum(self.stage_len)[:-1]:
+            a = int(a)
+            fits = [i for i, q in enumerate(cues) if len(q) <= a]
+            q = cues[fits[int(rng.integers(len(fits)))]]
+            b = int(rng.integers(B - 1 if prev_b >= 0 else B))
+            if prev_b >= 0 and b >= prev_b:
+                b += 1
+            stream[a - len(q):a, b] = q
+            planted.append(a - 1)
+            prev_b = b
+        return {"stream": stream, "cues": cues, "planted": np.asarray(planted, dtype=np.int64)}
 
     def layer(self, layer: int, cache_weights: bool = True) -> SyntheticLayer:
         """The layer's weights (router, experts); x and bias are per call."""
