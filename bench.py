@@ -393,6 +393,28 @@ def main() -> int:
     torch.cuda.synchronize()
     ms_no_events = (time.perf_counter() - t1) * 1e3 / args.steps
 
+    # the same calls replayed from a HIP graph: one capture of one call per weight copy
+    side = torch.cuda.Stream()
+    side.wait_stream(stream)
+    with torch.cuda.stream(side):
+        for a in plain:
+            moe.moe_layer_forward(a, dev.ws)
+    stream.wait_stream(side)
+    torch.cuda.synchronize()
+    graph = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(graph):
+        for a in plain:
+            moe.moe_layer_forward(a, dev.ws)
+    reps = max(1, args.steps // len(plain))
+    graph.replay()
+    torch.cuda.synchronize()
+    t2 = time.perf_counter()
+    for _ in range(reps):
+        graph.replay()
+    torch.cuda.synchronize()
+    ms_graph = (time.perf_counter() - t2) * 1e3 / (reps * len(plain))
+    del graph
+
     # streaming-read reference of this GPU: one pass of 16-byte loads over 4 GiB
     probe_src = torch.empty(1 << 30, dtype=torch.float32, device="cuda")
     probe_sink = torch.zeros(1, dtype=torch.int32, device="cuda")
@@ -459,6 +481,8 @@ def main() -> int:
         "stages_us_instrumented": stage_us,
         "step_us_instrumented": step_pct,
         "ms_per_step_without_events": ms_no_events,
+        # the same calls replayed from a HIP graph (one graph launch per call instead of 5-6 kernel launches)
+        "ms_per_step_graph": ms_graph,
         "hbm_read_probe_GBps": read_probe_gbps,
         "mfma_tflops_layer_algorithmic": alg["flops"] / (ms_per_step * 1e-3) / 1e12,
         # whole layer against its roofline: the slower of moving its algorithmic bytes at
