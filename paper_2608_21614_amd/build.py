@@ -15,7 +15,7 @@ CSRC = os.path.join(HERE, "csrc")
 LIB = os.path.join(HERE, "libsaem_moe.so")
 BUILD_DIR = os.path.join(HERE, "_build")
 SOURCES = ["abi.hip", "route.hip", "repack.hip", "ffn.hip", "combine.hip", "pack.hip", "probe.hip"]
-HOST_SOURCES = ["host_ffn.cpp", "cue_fsm.cpp"]   # host-only C++ (system compiler)
+HOST_SOURCES = ["host_abi.cpp", "host_ffn.cpp", "cue_fsm.cpp"]   # host-only C++ (system compiler)
 ARCH = "gfx950"
 
 HIPCC_FLAGS = [

@@ -1,6 +1,7 @@
-// abi.hip -- the C ABI of libsaem_moe.so: host-side validation, workspace
-// layout and launch sequencing.  Every check runs on the host before anything
-// is enqueued and never touches device memory.
+// abi.hip -- the C ABI of libsaem_moe.so: argument checks, workspace layout and
+// launch sequencing of the device calls.  Every check runs on the host before
+// anything is enqueued and never touches device memory; the shape rules
+// (moe_check_dims) and the other host-only calls are in host_abi.cpp.
 #include <string.h>
 
 #include <algorithm>
@@ -11,8 +12,6 @@
 namespace {
 
 using saem::Shape;
-
-constexpr long long kMaxRows = 1ll << 24;  // T*k + S*T rows handled by one call
 
 // Arrays read or written with 16-byte vector accesses (activations, weights,
 // outputs, workspace) must be 16-byte aligned; index, count and gate arrays only
@@ -27,24 +26,6 @@ bool ok_arr(const void* p, long long n) { return n == 0 ? aligned16(p) : ok_ptr(
 bool ok_ptr4(const void* p) { return p != nullptr && aligned4(p); }
 bool ok_opt4(const void* p) { return p == nullptr || aligned4(p); }
 bool ok_arr4(const void* p, long long n) { return n == 0 ? aligned4(p) : ok_ptr4(p); }
-
-moe_status check_dims(const moe_dims* d) {
-    if (!d) return MOE_ERR_INVALID_ARG;
-    if (d->tokens < 0 || d->hidden <= 0 || d->experts <= 0 || d->ffn <= 0 || d->top_k <= 0 || d->shared < 0 ||
-        d->slots < 0)
-        return MOE_ERR_INVALID_ARG;
-    if (d->dtype != MOE_F32 && d->dtype != MOE_BF16) return MOE_ERR_INVALID_ARG;
-    if (d->top_k > d->experts || d->slots > d->experts) return MOE_ERR_INVALID_ARG;
-    if (d->shared > 0 && d->shared_ffn <= 0) return MOE_ERR_INVALID_ARG;
-    if (d->experts > 256 || d->top_k > 8 || d->shared > 8) return MOE_ERR_UNSUPPORTED;
-    if (d->hidden % 64 != 0 || d->ffn % 64 != 0) return MOE_ERR_UNSUPPORTED;
-    if (d->shared > 0 && d->shared_ffn % 64 != 0) return MOE_ERR_UNSUPPORTED;
-    const long long rows = (long long)d->tokens * d->top_k + (long long)d->shared * d->tokens;
-    if (rows > kMaxRows) return MOE_ERR_UNSUPPORTED;
-    if ((long long)d->hidden > (1 << 20) || (long long)d->ffn > (1 << 20) || (long long)d->shared_ffn > (1 << 20))
-        return MOE_ERR_UNSUPPORTED;
-    return MOE_OK;
-}
 
 Shape shape_of(const moe_dims* d) {
     Shape s;
@@ -107,23 +88,10 @@ moe_status hip_status(hipError_t e) { return e == hipSuccess ? MOE_OK : MOE_ERR_
 
 extern "C" {
 
-int moe_abi_version(void) { return MOE_ABI_VERSION; }
 
-const char* moe_status_str(moe_status s) {
-    switch (s) {
-        case MOE_OK: return "ok";
-        case MOE_ERR_INVALID_ARG: return "invalid argument";
-        case MOE_ERR_UNSUPPORTED: return "unsupported shape or option";
-        case MOE_ERR_WORKSPACE: return "workspace missing or too small";
-        case MOE_ERR_HIP: return "HIP launch or runtime error";
-    }
-    return "unknown status";
-}
-
-moe_status moe_check_dims(const moe_dims* dims) { return check_dims(dims); }
 
 moe_status moe_workspace_bytes(const moe_dims* dims, size_t* bytes) {
-    const moe_status st = check_dims(dims);
+    const moe_status st = moe_check_dims(dims);
     if (st != MOE_OK) return st;
     if (!bytes) return MOE_ERR_INVALID_ARG;
     *bytes = layout_of(shape_of(dims)).total;
@@ -133,7 +101,7 @@ moe_status moe_workspace_bytes(const moe_dims* dims, size_t* bytes) {
 moe_status moe_route_topk(const moe_dims* dims, const void* x, const void* w_router, const float* bias,
                           float* logits, uint32_t flags, int32_t* topk_idx, float* topk_w, void* ws, size_t ws_bytes,
                           void* stream) {
-    moe_status st = check_dims(dims);
+    moe_status st = moe_check_dims(dims);
     if (st != MOE_OK) return st;
     if (flags & ~MOE_LOGITS_IN) return MOE_ERR_INVALID_ARG;
     const bool lin = (flags & MOE_LOGITS_IN) != 0;
@@ -151,7 +119,7 @@ moe_status moe_repack(const moe_dims* dims, const int32_t* topk_idx, const float
                       const int32_t* expert_slot, const void* x, int32_t* counts, int32_t* seg_start,
                       int32_t* perm, int32_t* inv_perm, int32_t* n_res, void* off_rows, float* off_w,
                       void* stream) {
-    moe_status st = check_dims(dims);
+    moe_status st = moe_check_dims(dims);
     if (st != MOE_OK) return st;
     const long long T = dims->tokens;
     if (!ok_arr4(topk_idx, T) || !ok_ptr4(expert_slot) || !ok_ptr4(counts) || !ok_ptr4(seg_start) ||
@@ -169,7 +137,7 @@ moe_status moe_repack(const moe_dims* dims, const int32_t* topk_idx, const float
 moe_status moe_grouped_ffn(const moe_dims* dims, const void* x, const int32_t* perm, const int32_t* counts,
                            const int32_t* seg_start, const int32_t* expert_slot, const void* w13, const void* w2,
                            const void* ws13, const void* ws2, float* y, void* ws, size_t ws_bytes, void* stream) {
-    moe_status st = check_dims(dims);
+    moe_status st = moe_check_dims(dims);
     if (st != MOE_OK) return st;
     const long long T = dims->tokens;
     if (!ok_arr(x, T) || !ok_arr4(perm, T) || !ok_ptr4(counts) || !ok_ptr4(seg_start) || !ok_ptr4(expert_slot) ||
@@ -198,7 +166,7 @@ moe_status moe_grouped_ffn(const moe_dims* dims, const void* x, const int32_t* p
 moe_status moe_combine(const moe_dims* dims, const int32_t* topk_idx, const float* topk_w,
                        const int32_t* inv_perm, const int32_t* expert_slot, const float* y,
                        const float* y_off, const int32_t* n_res, void* out, int32_t out_dtype, void* stream) {
-    moe_status st = check_dims(dims);
+    moe_status st = moe_check_dims(dims);
     if (st != MOE_OK) return st;
     if (out_dtype != MOE_F32 && out_dtype != MOE_BF16) return MOE_ERR_INVALID_ARG;
     const long long T = dims->tokens;
@@ -214,7 +182,7 @@ moe_status moe_combine(const moe_dims* dims, const int32_t* topk_idx, const floa
 moe_status moe_layer_forward(const moe_layer_args* a, void* ws, size_t ws_bytes, void* stream) {
     if (!a || a->struct_size != sizeof(moe_layer_args)) return MOE_ERR_INVALID_ARG;
     const moe_dims* d = &a->dims;
-    moe_status st = check_dims(d);
+    moe_status st = moe_check_dims(d);
     if (st != MOE_OK) return st;
     if (a->flags & ~MOE_LOGITS_IN) return MOE_ERR_INVALID_ARG;
     if (a->out_dtype != MOE_F32 && a->out_dtype != MOE_BF16) return MOE_ERR_INVALID_ARG;
@@ -307,35 +275,6 @@ moe_status moe_stage_accumulate(int32_t experts, const int32_t* counts, int64_t*
 moe_status moe_read_probe(const void* src, int64_t bytes, uint32_t* sink, void* stream) {
     if (bytes < 0 || bytes % 16 != 0 || (bytes > 0 && !ok_ptr(src)) || !ok_ptr4(sink)) return MOE_ERR_INVALID_ARG;
     return hip_status(saem::launch_read_probe(src, bytes, sink, static_cast<hipStream_t>(stream)));
-}
-
-moe_status moe_stage_plan(int32_t experts, int32_t slots, const int64_t* log, const int32_t* prev_slot,
-                          int32_t* new_slot) {
-    if (experts <= 0 || experts > 256 || slots < 0 || slots > experts || !log || !prev_slot || !new_slot)
-        return MOE_ERR_INVALID_ARG;
-    int order[256];
-    for (int e = 0; e < experts; ++e) order[e] = e;
-    std::stable_sort(order, order + experts, [&](int a, int b) { return log[a] > log[b]; });
-    bool keep[256] = {false};
-    for (int i = 0; i < slots; ++i) keep[order[i]] = true;
-    bool used[256] = {false};
-    for (int e = 0; e < experts; ++e) {
-        new_slot[e] = -1;
-        const int ps = prev_slot[e];
-        if (keep[e] && ps >= 0 && ps < slots && !used[ps]) {
-            new_slot[e] = ps;
-            used[ps] = true;
-        }
-    }
-    int next_free = 0;
-    for (int i = 0; i < slots; ++i) {
-        const int e = order[i];
-        if (new_slot[e] >= 0) continue;
-        while (next_free < slots && used[next_free]) ++next_free;
-        new_slot[e] = next_free;
-        used[next_free] = true;
-    }
-    return MOE_OK;
 }
 
 }  // extern "C"
