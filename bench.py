@@ -208,7 +208,7 @@ def bookkeeping_timings(dev, n: int):
             "timing": "wall clock per call, device synchronised before and after each call"}
 
 
-def trace_timings(seed: int, lags, detect: bool = False):
+def trace_timings(seed: int, lags, detect: bool = False, persistence: float = 0.0):
     """The stage-structured decode trace with real slot copies (Section IV-C), per prefetch lag.
 
     Routers, stage biases and per-call activations are the trace's own (so the
@@ -222,8 +222,9 @@ def trace_timings(seed: int, lags, detect: bool = False):
     import torch
     from paper_2608_21614_amd.device import to_device
     from paper_2608_21614_amd.residency import StageResidencyRunner
+    from dataclasses import replace
     from workloads import TRACE, StageTrace
-    c = TRACE
+    c = replace(TRACE, stage_persistence=persistence)
     trace = StageTrace(c, seed=seed)
     L, E = c.layers, c.experts
     layers = [trace.layer(l, cache_weights=False) for l in range(L)]
@@ -233,6 +234,7 @@ def trace_timings(seed: int, lags, detect: bool = False):
         xs.append(to_device(np.stack([trace.x(s, l) for s in range(c.steps)])))   # [steps, T, H] on the device
     base13, base2 = layers[0].w13(0), layers[0].w2(0)
     out = {"steps": c.steps, "layers": L, "stages": int(trace.n_stages), "batch": c.batch, "slots": c.n_slots,
+           "stage_persistence": persistence,
            "weights": "one seeded expert's weights in every (layer, expert) host buffer", "runs": []}
     detector = None
     if detect:
@@ -251,10 +253,18 @@ def trace_timings(seed: int, lags, detect: bool = False):
             runner.reset(lag)
         r = runner.run(detector=detector)
         calls = r["calls"]
+        if "tc_seq" not in out:   # routing, hence the stage activation matrices, does not depend on the lag
+            from paper_2608_21614_amd.stage_trace import clairvoyant_chr, temporal_coherence
+            out["tc_seq"] = temporal_coherence(r["counts"], trace.stage_len)
+            out["chr_clairvoyant"] = clairvoyant_chr(r["counts"], trace.stage_len, c.n_slots)
+            if detect:
+                edges = np.concatenate([[0], r["boundary_steps"] + 1, [c.steps]])
+                out["tc_seq_detected_stages"] = temporal_coherence(r["counts"], np.diff(edges))
         out["runs"].append({"lag": lag, "trace_ms": r["trace_ms"], "us_per_layer_call": r["trace_ms"] * 1e3 / calls,
                             "chr_online": r["chr_online"], "copied_experts": r["copied_experts"],
                             "copy_ms_total": r["copy_ms_total"], "copy_GBps": r["copy_GBps"],
-                            "stall_ms_total": r["stall_ms_total"], "boundaries": int(len(r["boundary_steps"]))})
+                            "stall_ms_total": r["stall_ms_total"], "boundaries": int(len(r["boundary_steps"])),
+                            "eta_chr": r["chr_online"] / out["chr_clairvoyant"]})
         log(f"[bench]   {out['runs'][-1]}")
     return out
 
@@ -281,6 +291,9 @@ def main() -> int:
     ap.add_argument("--trace", type=str, default="", metavar="LAGS",
                     help="with --workload c5_stage_trace: also run the whole stage-structured trace with real "
                          "slot copies, once per comma-separated prefetch lag (e.g. 0,8); extra object")
+    ap.add_argument("--trace-persistence", type=float, default=0.0, metavar="RHO",
+                    help="with --trace: each stage's expert popularity is RHO x the previous stage's + (1 - RHO) x "
+                         "a fresh Dirichlet draw (0, the default: independent stages)")
     ap.add_argument("--detect", action="store_true",
                     help="with --trace: stage boundaries from the cue machine on the generated tokens "
                          "(Section IV-B.1) instead of the trace's true stage ends")
@@ -497,7 +510,8 @@ def main() -> int:
     if args.trace:
         del copies, dev
         torch.cuda.empty_cache()
-        result["trace"] = trace_timings(args.seed, [int(v) for v in args.trace.split(",")], args.detect)
+        result["trace"] = trace_timings(args.seed, [int(v) for v in args.trace.split(",")], args.detect,
+                                        args.trace_persistence)
     if not args.no_cpu_baseline:
         log("[bench] timing the CPU oracle")
         result["cpu_baseline"] = cpu_baseline(layer, args.cpu_seconds)

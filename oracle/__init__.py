@@ -457,3 +457,43 @@ def stage_lengths_from_events(matched: np.ndarray, steps: int) -> np.ndarray:
     cuts = [int(i) + 1 for i in ev if int(i) + 1 < steps]
     edges = [0] + cuts + [steps]
     return np.diff(np.asarray(edges, dtype=np.int64))
+
+
+def temporal_coherence(counts: np.ndarray, stage_len: np.ndarray) -> float:
+    """TC_seq (Section III, Motivation 2, the TC_seq equation), written as defined.
+
+    R^p[l, e] = tokens of stage p routed to expert e of layer l / tokens layer l
+    processed in stage p; sim(R^p, R^{p+1}) = (1/L) sum_l cos(R^p_l, R^{p+1}_l);
+    TC_seq = 1/(P-1) sum_{p=1}^{P-1} sim(R^p, R^{p+1}).  counts[step, l, e] are
+    routed pairs, and every step processes the same number of tokens in every
+    layer, so a layer's tokens in a stage are its pairs / k = its step count x
+    batch; the division is done as written even though cosines ignore it.
+    NaN for fewer than two stages.
+    """
+    c = np.asarray(counts, dtype=np.int64)
+    steps, L, E = c.shape
+    P = len(stage_len)
+    if P < 2:
+        return float("nan")
+    R = []
+    a = 0
+    for n in stage_len:
+        b = a + int(n)
+        m = np.zeros((L, E))
+        for l in range(L):
+            tot = sum(int(c[s, l, e]) for s in range(a, b) for e in range(E))
+            for e in range(E):
+                m[l, e] = sum(int(c[s, l, e]) for s in range(a, b)) / tot
+        R.append(m)
+        a = b
+    total = 0.0
+    for p in range(P - 1):
+        sim = 0.0
+        for l in range(L):
+            u, v = R[p][l], R[p + 1][l]
+            dot = sum(u[e] * v[e] for e in range(E))
+            nu = sum(u[e] * u[e] for e in range(E)) ** 0.5
+            nv = sum(v[e] * v[e] for e in range(E)) ** 0.5
+            sim += dot / (nu * nv)
+        total += sim / L
+    return total / (P - 1)

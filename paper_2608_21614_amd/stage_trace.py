@@ -79,3 +79,43 @@ def run_routing_trace(trace, routers, device="cuda", log_every: int = 0, x_of=No
     total = int(cnt.sum())
     return {"counts": cnt, "n_res": nr, "topk_idx": to_host(idx), "slot_history": hist,
             "chr_online": float(nr.sum()) / total if total else 1.0}
+
+
+def temporal_coherence(counts: np.ndarray, stage_len: np.ndarray) -> float:
+    """Sequence-level temporal coherence TC_seq of a routed trace (Section III, Motivation 2).
+
+    counts[step, layer, e]: routed pairs per expert of every (step, layer) call.
+    A stage's activation matrix has one row per layer: the fraction of the
+    layer's routed tokens that went to each expert over the stage.  TC_seq is
+    the mean, over consecutive stages, of the layer-averaged cosine similarity
+    of their rows (cosines do not depend on how each row is normalised, so the
+    per-stage counts serve directly).  NaN for a trace of one stage.
+    """
+    c = np.asarray(counts, dtype=np.float64)
+    ends = np.cumsum(np.asarray(stage_len, dtype=np.int64))
+    starts = ends - np.asarray(stage_len, dtype=np.int64)
+    if len(ends) < 2:
+        return float("nan")
+    R = np.stack([c[a:b].sum(axis=0) for a, b in zip(starts, ends)])     # [P, L, E]
+    norm = np.linalg.norm(R, axis=2)                                     # [P, L]
+    cos = (R[:-1] * R[1:]).sum(axis=2) / (norm[:-1] * norm[1:])          # [P-1, L]
+    return float(cos.mean(axis=1).mean())
+
+
+def clairvoyant_chr(counts: np.ndarray, stage_len: np.ndarray, n_slots: int) -> float:
+    """Cache-hit ratio of the prediction oracle of Section V-C: every stage runs with
+    the residency planned from its own activation log (its n_slots most used experts
+    per layer, ties to the lower id), the upper bound of the online policy."""
+    c = np.asarray(counts, dtype=np.int64)
+    ends = np.cumsum(np.asarray(stage_len, dtype=np.int64))
+    starts = ends - np.asarray(stage_len, dtype=np.int64)
+    total = int(c.sum())
+    if total == 0:
+        return 1.0
+    hits = 0
+    for a, b in zip(starts, ends):
+        log = c[a:b].sum(axis=0)                                    # [L, E]
+        for row in log:
+            order = np.lexsort((np.arange(row.size), -row))        # count descending, then id ascending
+            hits += int(row[order[:n_slots]].sum())
+    return hits / total

@@ -161,6 +161,9 @@ class TraceConfig:
     n_slots: int = 2                 # resident experts per layer (25% ECR)
     dirichlet_alpha: float = 0.3
     mean_stage_len: float = 256.0
+    # 0: every (stage, layer) popularity is an independent draw; rho > 0: stage s's
+    # popularity is rho x stage s-1's + (1 - rho) x a fresh draw (more coherent stages)
+    stage_persistence: float = 0.0
     x_std: float = 1.0
     w_std: float = 0.02
     dtype: str = "bf16"
@@ -330,9 +333,13 @@ class StageTrace:
         self.stage_len = np.asarray(lens, dtype=np.int64)
         scale = _gumbel_scale(c.logit_std())
         bias = np.empty((len(lens), c.layers, c.experts), dtype=np.float32)
+        prev = [None] * c.layers
         for s in range(len(lens)):
             for l in range(c.layers):
                 p = _rng(self.seed, l, _TAG_DIR, s).dirichlet(np.full(c.experts, c.dirichlet_alpha))
+                if c.stage_persistence > 0 and prev[l] is not None:
+                    p = c.stage_persistence * prev[l] + (1.0 - c.stage_persistence) * p
+                prev[l] = p
                 p = np.maximum(p, 1e-6)
                 bias[s, l] = (scale * np.log(p)).astype(np.float32)
         self.stage_bias = bias
