@@ -149,3 +149,16 @@ def test_machine_rejects_bad_input():
     m = np.zeros(1, dtype=np.int32)
     assert lib.moe_cue_step(fsm.ctypes.data, 1, None, st.ctypes.data, m.ctypes.data) == saem.MOE_ERR_INVALID_ARG
     assert lib.moe_cue_step(fsm.ctypes.data, 0, None, None, None) == saem.MOE_OK
+
+
+@pytest.mark.parametrize("batch,mean", [(16, 2.0), (1, 1.5)])
+def test_planted_cues_survive_short_stages(batch, mean):
+    """Cues planted at boundaries a step or two apart never overwrite one another."""
+    from dataclasses import replace
+    cfg = replace(workloads.TRACE, steps=300, batch=batch, mean_stage_len=mean)
+    for seed in range(6):
+        ts = workloads.StageTrace(cfg, seed).token_stream()
+        got = _run_machine(ts["cues"], ts["stream"])
+        assert np.array_equal(got, oracle.cue_matches(ts["cues"], ts["stream"]))
+        events = set(np.flatnonzero((got >= 0).any(axis=1)).tolist())
+        assert set(ts["planted"].tolist()) <= events, seed

@@ -390,11 +390,12 @@ class StageTrace:
         """Generated tokens of the batch, [steps, batch] int32, with the cues planted at the boundaries.
 
         Background tokens are Zipf(token_zipf_s) over the vocabulary.  For every
-        stage after the first, one sequence (seeded, never the one of the
-        previous boundary) generates a cue whose last token falls on the last
-        step of the previous stage, so a detector that matches cues sees the
-        transition exactly at the planted boundary.  Returns stream, cues and
-        planted (the step of each planted cue's last token).
+        stage after the first, one sequence (seeded, among those whose last
+        planted cue ends before this one starts, so no cue overwrites another)
+        generates a cue whose last token falls on the last step of the previous
+        stage, so a detector that matches cues sees the transition exactly at
+        the planted boundary.  Returns stream, cues and planted (the step of
+        each planted cue's last token).
         """
         c = self.cfg
         steps, B = c.steps, c.batch
@@ -406,17 +407,19 @@ class StageTrace:
         cues = self.cues()
         rng = _rng(self.seed, 0, _TAG_PLANT, 0)
         planted = []
-        prev_b = -1
+        last_end = np.full(B, -1, dtype=np.int64)      # step of each sequence's last planted token
         for a in np.cumsum(self.stage_len)[:-1]:
             a = int(a)
             fits = [i for i, q in enumerate(cues) if len(q) <= a]
             q = cues[fits[int(rng.integers(len(fits)))]]
-            b = int(rng.integers(B - 1 if prev_b >= 0 else B))
-            if prev_b >= 0 and b >= prev_b:
-                b += 1
+            free = np.flatnonzero(last_end < a - len(q))
+            if free.size == 0:     # boundaries too close for this cue: the one-token cue always fits
+                q = cues[0]
+                free = np.flatnonzero(last_end < a - 1)
+            b = int(free[int(rng.integers(free.size))])
             stream[a - len(q):a, b] = q
+            last_end[b] = a - 1
             planted.append(a - 1)
-            prev_b = b
         return {"stream": stream, "cues": cues, "planted": np.asarray(planted, dtype=np.int64)}
 
     def layer(self, layer: int, cache_weights: bool = True) -> SyntheticLayer:
