@@ -437,11 +437,15 @@ __global__ void __launch_bounds__(256, 3) k_ffn_tiled(Args a, int max_rtiles, in
     __shared__ __attribute__((aligned(16))) uint16_t sW[16][512];
     __shared__ __attribute__((aligned(16))) uint16_t sX[kTn][kXPitch];
 
+    const int pid = blockIdx.x;
+    if (!kDown && pid >= grid8) {  // workgroups past the items pack the offloaded rows (phase 1 only)
+        pack_offloaded(a, pid - grid8, gridDim.x - grid8, 2);
+        return;
+    }
     const int nact = list_active(a, s_list, s_wsum);
     const int total_rt = list_tiles(a, s_list, s_wsum, s_tpre, nact);
     // XCD-aware order: workgroups are dealt to the 8 XCDs round-robin, so logical
     // items pid/8, pid/8 + 1, ... of one XCD are consecutive in this numbering.
-    const int pid = blockIdx.x;
     const int item = (pid % 8) * (grid8 / 8) + pid / 8;
     Group g;
     int mt_local, wn;
@@ -712,7 +716,7 @@ bool stream_weights(const Shape& s) {
 
 }  // namespace
 
-bool ffn_packs_offloaded(const Shape& s) { return use_stream(s); }
+bool ffn_packs_offloaded(const Shape& s) { return use_stream(s) || s.bf16; }
 
 int ffn_down_splits(const Shape& s) {
     if (!use_stream(s)) return 1;
@@ -801,9 +805,11 @@ hipError_t launch_grouped_ffn(const Shape& s, const FfnArgs& fa, hipStream_t st,
     {
         const int ntn_r = s.F / 64, ntn_s = s.S > 0 ? s.Fs / 64 : 1;
         const long long grid = round8((long long)max_rtiles * ntn_r + (long long)s.S * tps * ntn_s);
-        if (grid > 0)
-            hipLaunchKernelGGL((k_ffn_tiled<false>), dim3((unsigned)grid), dim3(256), 0, st, a, max_rtiles, ntn_r,
-                               ntn_s, (int)grid);
+        // pack workgroups after the items: dispatched last, they overlap the phase's tail
+        const int n_pack = (fa.off_rows || fa.off_w) ? (P < 256 ? P : 256) : 0;
+        if (grid + n_pack > 0)
+            hipLaunchKernelGGL((k_ffn_tiled<false>), dim3((unsigned)(grid + n_pack)), dim3(256), 0, st, a, max_rtiles,
+                               ntn_r, ntn_s, (int)grid);
     }
     if (hipError_t e = mark(); e != hipSuccess) return e;
     {

@@ -6,7 +6,8 @@
 // chunks of 1024 pairs, split into contiguous ranges over up to kRepackGroups
 // workgroups of 1024 threads; every workgroup counts the whole batch itself, so
 // none waits for another, and the result does not depend on the split.  A
-// second small kernel packs the offloaded rows for the host.
+// second small kernel packs the offloaded rows for the host when the FFN does
+// not (moe_repack on its own, fp32 prefill).
 #include "block_ops.hpp"
 #include "kernels.hpp"
 
