@@ -410,20 +410,16 @@ def cue_matches(cues: Sequence[Sequence[int]], stream: np.ndarray) -> np.ndarray
     there.  After every step the detector checks whether the window of recent
     tokens of each sequence ends with one of the cues (a cue being one or more
     token ids).  Written as that definition: every cue is compared with the
-    tail of every window.  Returns [steps, B] int32: the id of the longest cue
-    equal to the window's tail after the step (identical cues: the lowest id),
-    or -1 when none is.
+    last tokens of every sequence.  A cue's tokens are never negative, so a
+    cue cannot match across a step with no token (nor reach back before the
+    first step, padded with -2 below): that is the restart.  Returns [steps, B]
+    int32: the id of the longest cue equal to the window's tail after the step
+    (identical cues: the lowest id), or -1 when none is.
     """
     s = np.asarray(stream, dtype=np.int64)
     if s.ndim == 1:
         s = s[:, None]
     steps, B = s.shape
-    # tokens in the window after each step (since the last restart)
-    window = np.zeros((steps, B), dtype=np.int64)
-    run = np.zeros(B, dtype=np.int64)
-    for i in range(steps):
-        run = np.where(s[i] < 0, 0, run + 1)
-        window[i] = run
     best = np.full((steps, B), -1, dtype=np.int32)
     best_len = np.zeros((steps, B), dtype=np.int64)
     for cid, cue in enumerate(cues):
@@ -431,7 +427,7 @@ def cue_matches(cues: Sequence[Sequence[int]], stream: np.ndarray) -> np.ndarray
         L = len(c)
         if L == 0:
             continue
-        hit = window >= L
+        hit = np.ones((steps, B), dtype=bool)
         for j in range(L):           # token j of the cue sits L-1-j steps back
             back = L - 1 - j
             shifted = np.full((steps, B), -2, dtype=np.int64)

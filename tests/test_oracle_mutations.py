@@ -50,3 +50,38 @@ def test_pins_catch_planted_mistake(tmp_path, name, old, new):
                        cwd=ROOT, env=env, capture_output=True, text=True, timeout=600)
     assert r.returncode != 0, f"planted mistake '{name}' passed every pin:\n{r.stdout[-2000:]}"
     assert "failed" in r.stdout
+
+
+# The stage-boundary and coherence functions are Python; a mistake is planted in a copy
+# of the oracle package that shadows the real one for the pin tests' subprocess.
+PY_SRC = os.path.join(ROOT, "oracle", "__init__.py")
+PY_PINS = [os.path.join(ROOT, "tests", "test_cue_fsm.py"), os.path.join(ROOT, "tests", "test_temporal_coherence.py")]
+
+PY_MUTATIONS = [
+    ("cue ties go to the higher id", "take = hit & (L > best_len)", "take = hit & (L >= best_len)"),
+    ("first cue wins instead of the longest", "take = hit & (L > best_len)", "take = hit & (best < 0)"),
+    ("negative ids match a cue token", "hit &= shifted == c[j]", "hit &= (shifted == c[j]) | (shifted == -1)"),
+    ("cue compared in reverse order", "back = L - 1 - j", "back = j"),
+    ("stage cut one step early", "cuts = [int(i) + 1 for i in ev if int(i) + 1 < steps]",
+     "cuts = [int(i) for i in ev if 0 < int(i) < steps]"),
+    ("TC_seq averaged over P stages", "return total / (P - 1)", "return total / P"),
+    ("TC_seq without the cosine's norms", "sim += dot / (nu * nv)", "sim += dot"),
+    ("TC_seq compares with the last stage", "u, v = R[p][l], R[p + 1][l]", "u, v = R[p][l], R[-1][l]"),
+]
+
+
+@pytest.mark.parametrize("name,old,new", PY_MUTATIONS, ids=[m[0] for m in PY_MUTATIONS])
+def test_pins_catch_planted_python_mistake(tmp_path, name, old, new):
+    src = open(PY_SRC).read()
+    assert src.count(old) == 1, f"mutation anchor not unique: {old!r}"
+    pkg = tmp_path / "oracle"
+    pkg.mkdir()
+    (pkg / "__init__.py").write_text(src.replace(old, new))
+    env = dict(os.environ, MOE_ORACLE_LIB=os.path.join(ROOT, "oracle", "libmoe_oracle.so"),
+               PYTHONPATH=os.pathsep.join([str(tmp_path), ROOT]))
+    # run from the copy's directory: it comes first on sys.path, ahead of the repository
+    r = subprocess.run([sys.executable, "-m", "pytest", "-q", "-x", "-p", "no:cacheprovider", "--rootdir", ROOT,
+                        "-k", "oracle", *PY_PINS],
+                       cwd=str(tmp_path), env=env, capture_output=True, text=True, timeout=600)
+    assert r.returncode != 0, f"planted mistake '{name}' passed every pin:\n{r.stdout[-2000:]}"
+    assert "failed" in r.stdout
