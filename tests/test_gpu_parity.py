@@ -267,19 +267,19 @@ def test_layer_c1_tiny_f32(moe, seed):
     run_and_check_layer(moe, SyntheticLayer(CONFIGS["c1_tiny_f32"], seed))
 
 
-@pytest.mark.parametrize("seed", [0, 1])
+@pytest.mark.parametrize("seed", range(5))
 def test_layer_c2_mixtral_decode(moe, seed):
     say("layer c2_mixtral_decode seed", seed)
     run_and_check_layer(moe, SyntheticLayer(CONFIGS["c2_mixtral_decode"], seed))
 
 
-@pytest.mark.parametrize("seed", [0, 1, 2])
+@pytest.mark.parametrize("seed", range(5))
 def test_layer_c3_shared_decode(moe, seed):
     say("layer c3_shared_decode seed", seed)
     run_and_check_layer(moe, SyntheticLayer(CONFIGS["c3_shared_decode"], seed))
 
 
-@pytest.mark.parametrize("seed", [0, 1])
+@pytest.mark.parametrize("seed", range(5))
 def test_layer_c6_qwen3_decode(moe, seed):
     say("layer c6_qwen3_decode seed", seed)
     run_and_check_layer(moe, SyntheticLayer(CONFIGS["c6_qwen3_decode"], seed))
@@ -312,10 +312,11 @@ def test_layer_calls_share_one_workspace(moe):
             assert int(_host(o["n_res"])[0]) == ref["n_res"]
 
 
-def test_layer_c4_prefill_sampled(moe):
-    say("layer c4_prefill seed 0 (sampled tokens)")
-    lay = SyntheticLayer(CONFIGS["c4_prefill"], 0)
-    rng = np.random.default_rng(0)
+@pytest.mark.parametrize("seed", range(5))
+def test_layer_c4_prefill_sampled(moe, seed):
+    say("layer c4_prefill seed", seed, "(sampled tokens)")
+    lay = SyntheticLayer(CONFIGS["c4_prefill"], seed)
+    rng = np.random.default_rng(seed)
     sample = np.unique(np.concatenate([[0, 1, 2047], rng.choice(2048, 45, replace=False)]))
     run_and_check_layer(moe, lay, sample=sample)
 
