@@ -340,6 +340,10 @@ EDGE = [
     # 16-token router workgroup and the last 1024-pair repack chunk are all ragged
     (2049, 128, 64, 192, 6, 1, 64, "bf16", 40),
     (2049, 64, 8, 64, 2, 0, 0, "f32", 6),
+    # the ABI's limits at once: 256 experts, top-8, eight shared experts
+    (40, 128, 256, 64, 8, 8, 64, "bf16", 256),
+    (200, 128, 256, 64, 8, 8, 128, "bf16", 128),
+    (24, 64, 16, 64, 8, 8, 64, "f32", 8),
 ]
 
 
