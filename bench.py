@@ -116,18 +116,47 @@ def cpu_baseline(layer, seconds: float):
     oracle.layer_forward_synthetic(layer, offloaded=False)
     el1 = time.perf_counter() - t1
     oracle.set_threads(n)
-    model = "unknown"
-    try:
-        with open("/proc/cpuinfo") as f:
-            model = next((l.split(":", 1)[1].strip() for l in f if l.startswith("model name")), model)
-    except OSError:
-        pass
+    # the full layer as well: every pair, resident or offloaded (about a tenth of the time above),
+    # after one untimed call that first touches the offloaded experts' weights
+    oracle.layer_forward_synthetic(layer, offloaded=True)
+    full_reps = 0
+    t2 = time.perf_counter()
+    while True:
+        oracle.layer_forward_synthetic(layer, offloaded=True)
+        full_reps += 1
+        el2 = time.perf_counter() - t2
+        if el2 >= seconds / 10:
+            break
     return {"value": toks / el, "unit": "tokens/s", "cores": n, "kind": "oracle",
             "sample": f"{reps} full batch(es) of {layer.cfg.tokens} tokens of the same layer (resident experts + "
                       f"router + repack, fp64 C with OpenMP), {el:.1f} s",
             "single_thread": {"value": layer.cfg.tokens / el1, "unit": "tokens/s",
                               "sample": f"1 batch of {layer.cfg.tokens} tokens, {el1:.1f} s"},
-            "cpu_model": model, "logical_cpus_visible": os.cpu_count()}
+            "full_layer": {"value": full_reps * layer.cfg.tokens / el2, "unit": "tokens/s",
+                           "sample": f"{full_reps} batch(es) with the offloaded experts too, {el2:.1f} s"},
+            **host_cpu_info()}
+
+
+def host_cpu_info():
+    """CPU model, sockets and cores of this host (from /proc/cpuinfo), and the logical CPUs visible."""
+    model, sockets, cores = "unknown", set(), set()
+    try:
+        with open("/proc/cpuinfo") as f:
+            phys = "0"
+            for line in f:
+                key, _, val = line.partition(":")
+                key, val = key.strip(), val.strip()
+                if key == "model name" and model == "unknown":
+                    model = val
+                elif key == "physical id":
+                    phys = val
+                    sockets.add(val)
+                elif key == "core id":
+                    cores.add((phys, val))
+    except OSError:
+        pass
+    return {"cpu_model": model, "sockets": len(sockets) or None, "physical_cores": len(cores) or None,
+            "logical_cpus_visible": os.cpu_count(), "threads_allowed": len(os.sched_getaffinity(0))}
 
 
 # rates of this machine (MI355X box, 16 host threads): host->device copies, the host FFN on
