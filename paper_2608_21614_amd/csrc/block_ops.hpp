@@ -237,7 +237,8 @@ constexpr int repack_lds_ints() {
 //      an expert: a stable counting sort with no global atomics, and the same
 //      result for any split of the chunks over workgroups.
 // The workgroup with c_begin == 0 also writes counts, seg_start and n_res.
-// ids outside [0, E) are dropped (inv_perm = -1).
+// ids outside [0, E) are dropped (inv_perm = -1); the packed rows they leave
+// over at the end, [sum(counts), T*k), get perm = -1.
 template <int NT>
 __device__ inline void repack_chunks(int T, int E, int k, int slots, int c_begin, int c_end,
                                      const int32_t* __restrict__ idx, const int32_t* __restrict__ expert_slot,
@@ -290,6 +291,7 @@ __device__ inline void repack_chunks(int T, int E, int k, int slots, int c_begin
             }
         }
         const int rtot = __shfl(rinc, 63, 64);
+        const int otot = __shfl(oinc, 63, 64);
         int rp = rinc - rs, op = rtot + (oinc - os);
 #pragma unroll
         for (int i = 0; i < 4; ++i) {
@@ -304,7 +306,10 @@ __device__ inline void repack_chunks(int T, int E, int k, int slots, int c_begin
                 }
             }
         }
-        if (lane == 0) *s_nres = rtot;
+        if (lane == 0) {
+            s_nres[0] = rtot;
+            s_nres[1] = rtot + otot;  // valid pairs: the packed rows that get a pair
+        }
     }
     __syncthreads();
     if (c_begin == 0) {
@@ -312,7 +317,10 @@ __device__ inline void repack_chunks(int T, int E, int k, int slots, int c_begin
             counts[e] = s_cnt[e];
             seg_start[e] = s_base[e];
         }
-        if (tid == 0) *n_res = *s_nres;
+        if (tid == 0) *n_res = s_nres[0];
+        // rows past the valid pairs (there are some only when ids outside [0, E) were
+        // dropped) get no pair: mark them, so no reader takes a stale entry for one
+        for (int p = s_nres[1] + tid; p < P; p += NT) perm[p] = -1;
     }
     for (int e = tid; e < E; e += NT) s_base[e] += s_pre[e];
 

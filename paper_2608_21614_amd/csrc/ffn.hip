@@ -415,7 +415,12 @@ __device__ int list_tiles(const Args& a, int* s_list, int* s_wsum, int* s_tpre, 
             if (gi <= nact) s_tpre[gi] = run;
             run += v[i];
         }
-        if (lane == 63) s_wsum[0] = inc;
+        // the end entry: written above for nact < 256 (its run is then the total); with all
+        // 256 experts active it lies past the lanes' entries, so lane 63 writes it
+        if (lane == 63) {
+            s_wsum[0] = inc;
+            s_tpre[nact] = inc;
+        }
     }
     __syncthreads();
     return s_wsum[0];
@@ -573,6 +578,7 @@ __global__ void __launch_bounds__(256, 3) k_ffn_tiled(Args a, int max_rtiles, in
             for (int m = 0; m < 2; ++m) {
                 const f32x4 gv = acc[m][j], uv = acc[m + 2][j];
                 const int f = wrow0 + 16 * (2 * wr + m) + 4 * (lane >> 4);
+                if (f >= g.Fg) continue;
                 u32x2 packed;
                 packed.x = pack_bf16x2(silu(gv.x) * uv.x, silu(gv.y) * uv.y);
                 packed.y = pack_bf16x2(silu(gv.z) * uv.z, silu(gv.w) * uv.w);

@@ -114,7 +114,7 @@ class StageResidencyRunner:
     # -- trace ------------------------------------------------------------------
     def run(self, steps: Optional[int] = None, keep_outputs=(), log_every: int = 0,
             detector: Optional[dict] = None) -> dict:
-        """Runs the first `steps` steps.  keep_outputs: (step, layer) pairs whose outputs are kept.
+        """Runs the first `steps` steps.  keep_outputs: (step, layer) pairs whose outputs (and routing) are kept.
 
         Stage boundaries: without a detector, the trace's own stage ends.  With
         ``detector = {"cues": [...], "stream": [steps, batch] int32}`` they come
@@ -137,6 +137,7 @@ class StageResidencyRunner:
         counts = torch.empty((steps, L, E), dtype=torch.int32, device=self.device)
         n_res = torch.empty((steps, L), dtype=torch.int32, device=self.device)
         kept = {}
+        kept_idx = {}
         keep = set(keep_outputs)
         used_slot = np.empty((steps, L, E), dtype=np.int32)  # map each call ran with
         cur = self.slot.copy()          # map on the device now
@@ -175,13 +176,17 @@ class StageResidencyRunner:
                 x = self.x_of(step, l)
                 if not isinstance(x, torch.Tensor):
                     x = to_device(np.asarray(x), self.device)
-                out = torch.empty_like(self.out) if (step, l) in keep else self.out
+                kept_call = (step, l) in keep
+                out = torch.empty_like(self.out) if kept_call else self.out
+                idx = torch.empty((T, k), dtype=torch.int32, device=self.device) if kept_call else None
                 args = layer_args(self.dims, x, self.wr[l], self.bias[s, l], self.d_slot[l], self.w13[l], self.w2[l],
-                                  None, None, out, self.dt, counts=counts[step, l], n_res=n_res[step, l:l + 1])
+                                  None, None, out, self.dt, topk_idx=idx, counts=counts[step, l],
+                                  n_res=n_res[step, l:l + 1])
                 moe_layer_forward(args, self.ws, main)
                 moe_stage_accumulate(E, counts[step, l], self.log[l], main)
-                if (step, l) in keep:
+                if kept_call:
                     kept[(step, l)] = out
+                    kept_idx[(step, l)] = idx
             used_slot[step] = cur
             if detector is not None:
                 boundary = bool((moe_cue_step(fsm, tokens[step], cue_state) >= 0).any())
@@ -234,7 +239,7 @@ class StageResidencyRunner:
         total = int(cnt.sum())
         return {
             "counts": cnt, "n_res": nr, "used_slot": used_slot, "slot_history": np.stack(hist),
-            "outputs": kept,
+            "outputs": kept, "topk_idx": {key: to_host(v) for key, v in kept_idx.items()},
             "chr_online": float(nr.sum()) / total if total else 1.0,
             "trace_ms": ev0.elapsed_time(ev1), "calls": steps * L,
             "copied_experts": n_copied, "copy_ms_total": float(sum(copy_ms)),

@@ -11,6 +11,9 @@ Comparison rules
   (a perturbation below DELTA/2 can reorder it); the oracle enumerates them and
   the GPU's must be one of them; that token's expected output is then the
   oracle's under that routing.
+* Given identical scores -- the GPU's own fp32 scores, read back -- the GPU's
+  routing equals the oracle's top-k of those scores exactly.
+* Router scores: rel-L2 <= 1e-5 against the oracle's fp64 scores.
 * Float outputs: rel-L2 over the compared tensor, 1e-5 for fp32 layers and
   1e-2 for bf16 layers with fp32 accumulation.
 """
@@ -23,6 +26,7 @@ import oracle
 
 DELTA = 2e-4          # near-tie window of router scores (absolute)
 TOL = {"f32": 1e-5, "bf16": 1e-2}
+LOGIT_TOL = 1e-5      # rel-L2 of the fp32 router scores against the exact (fp64) scores
 
 
 def rel_l2(got, ref) -> float:
@@ -31,6 +35,15 @@ def rel_l2(got, ref) -> float:
     den = np.linalg.norm(ref)
     num = np.linalg.norm(got - ref)
     return float(num / den) if den > 0 else float(num)
+
+
+def row_rel_l2(got, ref) -> np.ndarray:
+    """rel-L2 of every row (a diagnostic next to the whole-tensor figure)."""
+    got = np.asarray(got, dtype=np.float64)
+    ref = np.asarray(ref, dtype=np.float64)
+    den = np.linalg.norm(ref, axis=-1)
+    num = np.linalg.norm(got - ref, axis=-1)
+    return np.where(den > 0, num / np.where(den > 0, den, 1.0), num)
 
 
 def host_f64(t: torch.Tensor) -> np.ndarray:

@@ -13,7 +13,8 @@ import pytest
 import torch
 
 import oracle
-from gpu_support import DELTA, TOL, check_offloaded_list, expected_routing, host_f64, rel_l2
+from gpu_support import (DELTA, LOGIT_TOL, TOL, check_offloaded_list, expected_routing, host_f64,
+                         rel_l2, row_rel_l2)
 from workloads import CONFIGS, SyntheticLayer, bf16_bits_to_f32, make_layer
 
 pytestmark = pytest.mark.gpu
@@ -188,6 +189,11 @@ def test_repack_bit_exact(moe, T, E, k, mode):
         np.testing.assert_array_equal(_host(counts), np.bincount(idx[valid], minlength=E))
         inv = _host(out["inv"])
         assert inv[3 * k] == -1 and inv[7 * k + 1] == -1
+        # the packed rows left over by the two dropped pairs hold no pair
+        perm = _host(out["perm"])
+        n_valid = int(valid.sum())
+        np.testing.assert_array_equal(perm[n_valid:P], -1)
+        assert sorted(perm[:n_valid].tolist()) == sorted(np.flatnonzero(valid.reshape(-1)).tolist())
         return
     ref = oracle.repack(idx, eff_res)
     np.testing.assert_array_equal(_host(counts), ref["counts"])
@@ -236,9 +242,16 @@ def run_and_check_layer(moe, lay, sample=None, check_off=True, offloaded_oracle=
     torch.cuda.synchronize()
     lg_ref = oracle.router_logits(lay.x, lay.w_router, lay.bias)
     lg = _host(o["logits"]).astype(np.float64)
+    idx = _host(o["topk_idx"])
     if T:
         assert np.abs(lg - lg_ref).max() < DELTA / 2, "router scores off by more than DELTA/2"
-    idx = _host(o["topk_idx"])
+        err_lg = rel_l2(lg, lg_ref)
+        say(f"  logits rel-L2 {err_lg:.3e} (tol {LOGIT_TOL})")
+        assert err_lg <= LOGIT_TOL
+        # given identical scores (the GPU's own fp32 logits), routing is bit-exact
+        own_idx, own_w = oracle.topk(lg, k)
+        np.testing.assert_array_equal(idx, own_idx)
+        np.testing.assert_allclose(_host(o["topk_w"]), own_w, rtol=2e-6, atol=1e-7)
     exp_idx, _ = expected_routing(lg_ref, idx, k) if T else (idx, {})
     np.testing.assert_array_equal(idx, exp_idx)
     ref = oracle.layer_forward_synthetic(lay, idx=exp_idx, sample=sample, offloaded=offloaded_oracle)
@@ -312,13 +325,56 @@ def test_layer_calls_share_one_workspace(moe):
             assert int(_host(o["n_res"])[0]) == ref["n_res"]
 
 
+def check_ffn_rows(moe, dev, lay, ref):
+    """The grouped FFN's rows (moe_grouped_ffn, the same kernels as the fused call) against the
+    oracle's expert outputs: every resident packed row, and every shared-expert row."""
+    c = lay.cfg
+    T, k, H, S = c.tokens, c.top_k, c.hidden, c.shared
+    o, y, _ = _standalone_chain(moe, dev)
+    torch.cuda.synchronize()
+    np.testing.assert_array_equal(_host(o["perm"])[: T * k], ref["perm"])
+    n_res = ref["n_res"]
+    yr = _host(y)
+    got, want = yr[:n_res], ref["y_rows"][:n_res]
+    err, worst = rel_l2(got, want), float(row_rel_l2(got, want).max()) if n_res else 0.0
+    say(f"  FFN rows: {n_res} resident rows rel-L2 {err:.3e}, worst row {worst:.3e}")
+    assert err <= TOL[c.dtype] and worst <= TOL[c.dtype]
+    toks = np.arange(T, dtype=np.int32)
+    for s_ in range(S):
+        want = oracle.expert_ffn(lay.x, toks, lay.ws13(s_), lay.ws2(s_))
+        got = yr[T * k + s_ * T: T * k + (s_ + 1) * T]
+        err, worst = rel_l2(got, want), float(row_rel_l2(got, want).max())
+        say(f"  FFN rows: shared expert {s_} rel-L2 {err:.3e}, worst row {worst:.3e}")
+        assert err <= TOL[c.dtype] and worst <= TOL[c.dtype]
+
+
 @pytest.mark.parametrize("seed", range(5))
-def test_layer_c4_prefill_sampled(moe, seed):
-    say("layer c4_prefill seed", seed, "(sampled tokens)")
+def test_layer_c4_prefill(moe, seed):
+    """The prefill config at full size: every token's output, and every FFN row."""
+    say("layer c4_prefill seed", seed, "(all 2048 tokens, all FFN rows)")
     lay = SyntheticLayer(CONFIGS["c4_prefill"], seed)
-    rng = np.random.default_rng(seed)
-    sample = np.unique(np.concatenate([[0, 1, 2047], rng.choice(2048, 45, replace=False)]))
-    run_and_check_layer(moe, lay, sample=sample)
+    dev, _, ref = run_and_check_layer(moe, lay)
+    check_ffn_rows(moe, dev, lay, ref)
+
+
+@pytest.mark.parametrize("name", ["c2_mixtral_decode", "c3_shared_decode"])
+def test_ffn_rows_decode(moe, name):
+    """Decode configs: every resident packed row and shared row of the grouped FFN (split-K sums added)."""
+    from paper_2608_21614_amd.device import DeviceLayer
+    say("FFN rows", name, "seed 1")
+    lay = SyntheticLayer(CONFIGS[name], 1)
+    dev, _, ref = run_and_check_layer(moe, lay)
+    check_ffn_rows(moe, dev, lay, ref)
+
+
+def test_layer_prefill_all_256_experts_active(moe):
+    """A prefill batch whose 256 experts are all resident and all receive tokens: the tiled
+    kernel's per-expert tile list then holds 256 groups (its end entry past the last lane's)."""
+    say("layer prefill, 256 experts all resident and active")
+    lay = make_layer(400, 64, 256, 64, 8, dtype="bf16", n_resident=256, residency="random", bias="none", seed=11)
+    dev, o, ref = run_and_check_layer(moe, lay)
+    assert (ref["counts"] > 0).all(), "every expert must be active for this case"
+    check_ffn_rows(moe, dev, lay, ref)
 
 
 EDGE = [

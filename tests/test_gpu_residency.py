@@ -10,7 +10,8 @@ test, since routing does not depend on residency):
 * the residency map each call ran with == oracle.stage_replay(..., lag)'s;
 * the resident pairs of every call and the online CHR;
 * every slot's bytes == the packed weights of the expert the plan put there;
-* the layer output of sampled calls == the oracle's resident partial sum.
+* the routing of sampled calls (near ties resolved to a valid alternative) and
+  their layer output == the oracle's resident partial sum under that routing.
 
 With ``detect``, the boundaries come from the cue machine fed the batch's
 generated tokens after every step (Section IV-B.1), on a token stream with a
@@ -27,7 +28,7 @@ import pytest
 import torch
 
 import oracle
-from gpu_support import TOL, host_f64, rel_l2
+from gpu_support import TOL, expected_routing, host_f64, rel_l2
 from workloads import TRACE, StageTrace
 
 pytestmark = pytest.mark.gpu
@@ -93,14 +94,14 @@ def test_stage_residency_with_slot_copies(lag, detect):
         x = trace.x(step, l)
         bias = trace.stage_bias[s, l]
         lg = oracle.router_logits(x, layers[l].w_router, bias)
-        idx, _ = oracle.topk(lg, k)
-        cnt = np.bincount(idx.ravel(), minlength=E)
-        if not np.array_equal(cnt, r["counts"][step, l]):       # a near tie the device resolved the other way
-            assert oracle.near_tie_alternatives(lg, k, 2e-4), f"step {step} layer {l}: counts differ without a near tie"
-            continue
+        idx_dev = r["topk_idx"][(step, l)]
+        # the device's routing: the oracle's, or (near-tied tokens) one of the valid alternatives
+        idx, alts = expected_routing(lg, idx_dev, k)
+        np.testing.assert_array_equal(idx_dev, idx)
+        np.testing.assert_array_equal(np.bincount(idx.ravel(), minlength=E), r["counts"][step, l])
         resident = r["used_slot"][step, l] >= 0
         ref_out = oracle.layer_forward(x, layers[l].w_router, bias, resident, k, layers[l].w13, layers[l].w2,
-                                       offloaded=False)
+                                       idx=idx, offloaded=False)
         err = rel_l2(host_f64(r["outputs"][(step, l)]), ref_out["out_res"])
         say(f"  step {step} layer {l}: resident {np.flatnonzero(resident).tolist()}, rel-L2 {err:.3e}")
         assert err <= TOL["bf16"]

@@ -76,13 +76,12 @@ def test_stage_trace_residency_and_chr(trace_run):
 def test_stage_trace_forward_first_and_last_step_of_every_stage(trace_run):
     """The full layer forward (resident partial) at the first and the last step of
     every stage, for the first and the last layer, with the residency in effect at
-    that step; the FFN output is checked on sampled tokens."""
+    that step; every token's output is checked."""
     from paper_2608_21614_amd.device import DeviceLayer, to_host
     cfg = TRACE
     trace, xs, gpu, ref, stage_of = (trace_run[n] for n in ("trace", "xs", "gpu", "ref", "stage_of"))
     ends = [int(v) for v in trace.stage_ends()]
     firsts = [0] + [e + 1 for e in ends[:-1]]
-    sample = np.array([0, cfg.batch // 2, cfg.batch - 1])
     for l in (0, cfg.layers - 1):
         lay = SyntheticLayer(cfg.layer_config(), 0, layer=l)      # expert weights cached across the calls
         for s in range(trace.n_stages):
@@ -98,10 +97,10 @@ def test_stage_trace_forward_first_and_last_step_of_every_stage(trace_run):
                 torch.cuda.synchronize()
                 idx = to_host(o["topk_idx"])
                 np.testing.assert_array_equal(idx, gpu["topk_idx"][step, l])
-                out = oracle.layer_forward_synthetic(lay, idx=idx, offloaded=False, sample=sample)
+                out = oracle.layer_forward_synthetic(lay, idx=idx, offloaded=False)
                 np.testing.assert_array_equal(to_host(o["counts"]), out["counts"])
                 assert int(to_host(o["n_res"])[0]) == int(gpu["n_res"][step, l])
-                err = rel_l2(host_f64(o["out"])[sample], out["out_res"])
+                err = rel_l2(host_f64(o["out"]), out["out_res"])
                 say(f"  layer {l} stage {s} step {step}: resident {np.flatnonzero(slot >= 0).tolist()}, "
                     f"rel-L2 {err:.3e}")
                 assert err <= TOL["bf16"]
