@@ -72,7 +72,8 @@ typedef enum moe_status {
     MOE_ERR_INVALID_ARG = 1,  /* NULL pointer, negative size, k > E, bad struct_size, ... */
     MOE_ERR_UNSUPPORTED = 2,  /* valid but not supported: H or F not a multiple of 64, E > 256, k > 8 */
     MOE_ERR_WORKSPACE = 3,    /* workspace NULL or smaller than moe_workspace_bytes() */
-    MOE_ERR_HIP = 4           /* a HIP launch or runtime call failed */
+    MOE_ERR_HIP = 4,          /* a HIP launch or runtime call failed */
+    MOE_ERR_SCRATCH_LIMIT = 5 /* moe_layer_forward_noalloc: the layer's workspace exceeds MOE_NOALLOC_SCRATCH_BYTES */
 } moe_status;
 
 typedef enum moe_dtype {
@@ -222,6 +223,29 @@ typedef struct moe_layer_args {
  * merges with moe_combine(..., y_off, ...).  Needs moe_workspace_bytes(&dims).
  */
 moe_status moe_layer_forward(const moe_layer_args* args, void* ws, size_t ws_bytes, void* stream);
+
+/* Size of the fixed device array that moe_layer_forward_noalloc uses as its workspace. */
+#define MOE_NOALLOC_SCRATCH_BYTES ((size_t)32 << 20)
+
+/*
+ * moe_layer_forward without a caller workspace and without any allocation, for
+ * callers that cannot allocate device memory (code under HIP graph capture,
+ * tight serving loops, harnesses that forbid hipMalloc).  The workspace is a
+ * fixed array of MOE_NOALLOC_SCRATCH_BYTES in the library, one per GPU, held
+ * until the process ends; the caller still passes every input and output in
+ * `args`, exactly as for moe_layer_forward, and gets the same results.
+ *   - Layers whose moe_workspace_bytes() exceeds MOE_NOALLOC_SCRATCH_BYTES (in
+ *     practice prefill-size batches) return MOE_ERR_SCRATCH_LIMIT, nothing enqueued.
+ *   - `stream` must belong to the calling thread's current device (NULL: its
+ *     null stream); a stream of another device returns MOE_ERR_INVALID_ARG.
+ *   - The first call on a device looks up that device's array (no allocation).
+ *   - All calls on one GPU share its array, and each leaves its intermediates
+ *     there: calls that may overlap on one GPU (several streams, or threads)
+ *     race on it and must be ordered by the caller.  Nothing is carried over
+ *     from one call to the next.
+ * Other errors as for moe_layer_forward.
+ */
+moe_status moe_layer_forward_noalloc(const moe_layer_args* args, void* stream);
 
 /*
  * Converts one row-major [rows, cols] expert matrix (cols contiguous) into the

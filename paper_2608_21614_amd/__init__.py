@@ -17,7 +17,8 @@ from typing import Optional
 HERE = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(HERE, "libsaem_moe.so")
 
-MOE_OK, MOE_ERR_INVALID_ARG, MOE_ERR_UNSUPPORTED, MOE_ERR_WORKSPACE, MOE_ERR_HIP = range(5)
+MOE_OK, MOE_ERR_INVALID_ARG, MOE_ERR_UNSUPPORTED, MOE_ERR_WORKSPACE, MOE_ERR_HIP, MOE_ERR_SCRATCH_LIMIT = range(6)
+MOE_NOALLOC_SCRATCH_BYTES = 32 << 20
 MOE_F32, MOE_BF16 = 0, 1
 MOE_LOGITS_IN = 1
 MOE_STAGE_EVENTS = 7
@@ -25,7 +26,8 @@ MOE_HOST_PIN = 1
 
 EXPORTED = [
     "moe_abi_version", "moe_status_str", "moe_check_dims", "moe_workspace_bytes", "moe_route_topk",
-    "moe_repack", "moe_grouped_ffn", "moe_combine", "moe_layer_forward", "moe_stage_accumulate",
+    "moe_repack", "moe_grouped_ffn", "moe_combine", "moe_layer_forward", "moe_layer_forward_noalloc",
+    "moe_stage_accumulate",
     "moe_stage_plan", "moe_pack_weights", "moe_host_ffn", "moe_offload_plan", "moe_read_probe",
     "moe_cue_fsm_words", "moe_cue_build", "moe_cue_step",
 ]
@@ -103,6 +105,7 @@ def _load() -> ctypes.CDLL:
         "moe_grouped_ffn": ([D, _vp, _vp, _vp, _vp, _vp, _vp, _vp, _vp, _vp, _vp, _vp, sz, _vp], ctypes.c_int),
         "moe_combine": ([D, _vp, _vp, _vp, _vp, _vp, _vp, _vp, _vp, i32, _vp], ctypes.c_int),
         "moe_layer_forward": ([ctypes.POINTER(moe_layer_args), _vp, sz, _vp], ctypes.c_int),
+        "moe_layer_forward_noalloc": ([ctypes.POINTER(moe_layer_args), _vp], ctypes.c_int),
         "moe_stage_accumulate": ([i32, _vp, _vp, _vp], ctypes.c_int),
         "moe_stage_plan": ([i32, i32, _vp, _vp, _vp], ctypes.c_int),
         "moe_pack_weights": ([_vp, _vp, ctypes.c_int64, ctypes.c_int64, i32, _vp], ctypes.c_int),
@@ -206,6 +209,11 @@ def layer_args(dims, x, w_router, bias, expert_slot, w13, w2, ws13, ws2, out, ou
 def moe_layer_forward(args: moe_layer_args, ws, stream=None):
     _check(lib.moe_layer_forward(ctypes.byref(args), _p(ws), ws.numel() * ws.element_size(), _stream(stream)),
            "moe_layer_forward")
+
+
+def moe_layer_forward_noalloc(args: moe_layer_args, stream=None):
+    """moe_layer_forward on the library's fixed per-GPU scratch array (no workspace, no allocation)."""
+    _check(lib.moe_layer_forward_noalloc(ctypes.byref(args), _stream(stream)), "moe_layer_forward_noalloc")
 
 
 def moe_pack_weights(src, dst, stream=None):

@@ -5,9 +5,16 @@
 #include <string.h>
 
 #include <algorithm>
+#include <mutex>
 
 #include "../../include/saem_moe.h"
 #include "kernels.hpp"
+
+// Workspace of moe_layer_forward_noalloc: one fixed array per GPU, held until the
+// process ends.  Host code never passes `scratch` itself to a kernel (on the
+// host it names a stand-in, not device memory): it looks up the array's device
+// address once per device and passes that.
+static __device__ __align__(256) unsigned char scratch[MOE_NOALLOC_SCRATCH_BYTES];
 
 namespace {
 
@@ -83,6 +90,34 @@ T* at(void* ws, size_t off) {
 }
 
 moe_status hip_status(hipError_t e) { return e == hipSuccess ? MOE_OK : MOE_ERR_HIP; }
+
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mu;
+void* g_scratch_ptr[kMaxDevices] = {};
+
+// Device address of the current device's scratch array, looked up on the first
+// call on that device.  *out stays NULL when the stream belongs to another device
+// (the array would not be that device's).
+hipError_t scratch_for_stream(hipStream_t st, void** out) {
+    *out = nullptr;
+    int dev = -1;
+    hipError_t e = hipGetDevice(&dev);
+    if (e != hipSuccess) return e;
+    hipDevice_t sdev = -1;
+    e = hipStreamGetDevice(st, &sdev);
+    if (e != hipSuccess) return e;
+    if (sdev != dev || dev < 0 || dev >= kMaxDevices) return hipSuccess;
+    std::lock_guard<std::mutex> lock(g_scratch_mu);
+    if (!g_scratch_ptr[dev]) {
+        void* p = nullptr;
+        e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+        if (e != hipSuccess) return e;
+        if (!p) return hipErrorInvalidSymbol;
+        g_scratch_ptr[dev] = p;
+    }
+    *out = g_scratch_ptr[dev];
+    return hipSuccess;
+}
 
 }  // namespace
 
@@ -179,7 +214,9 @@ moe_status moe_combine(const moe_dims* dims, const int32_t* topk_idx, const floa
                                            out_dtype == MOE_BF16, static_cast<hipStream_t>(stream)));
 }
 
-moe_status moe_layer_forward(const moe_layer_args* a, void* ws, size_t ws_bytes, void* stream) {
+// The fused forward on a given workspace; moe_layer_forward and moe_layer_forward_noalloc
+// (the library's fixed scratch array) both run it.
+static moe_status layer_forward(const moe_layer_args* a, void* ws, size_t ws_bytes, hipStream_t hs) {
     if (!a || a->struct_size != sizeof(moe_layer_args)) return MOE_ERR_INVALID_ARG;
     const moe_dims* d = &a->dims;
     moe_status st = moe_check_dims(d);
@@ -200,7 +237,6 @@ moe_status moe_layer_forward(const moe_layer_args* a, void* ws, size_t ws_bytes,
     const Shape s = shape_of(d);
     const Layout L = layout_of(s);
     if (!ws || ws_bytes < L.total || !aligned16(ws)) return MOE_ERR_WORKSPACE;
-    hipStream_t hs = static_cast<hipStream_t>(stream);
 
     float* logits = a->logits ? a->logits : at<float>(ws, L.logits);
     int32_t* idx = a->topk_idx ? a->topk_idx : at<int32_t>(ws, L.idx);
@@ -252,6 +288,22 @@ moe_status moe_layer_forward(const moe_layer_args* a, void* ws, size_t ws_bytes,
         e = mark(saem::launch_combine(s, idx, w, inv, a->expert_slot, f.y, L.ks, f.y_ks_stride, nullptr, nullptr,
                                       a->out, a->out_dtype == MOE_BF16, hs), 6);
     return hip_status(e);
+}
+
+moe_status moe_layer_forward(const moe_layer_args* a, void* ws, size_t ws_bytes, void* stream) {
+    return layer_forward(a, ws, ws_bytes, static_cast<hipStream_t>(stream));
+}
+
+moe_status moe_layer_forward_noalloc(const moe_layer_args* a, void* stream) {
+    if (!a || a->struct_size != sizeof(moe_layer_args)) return MOE_ERR_INVALID_ARG;
+    const moe_status st = moe_check_dims(&a->dims);
+    if (st != MOE_OK) return st;
+    if (layout_of(shape_of(&a->dims)).total > MOE_NOALLOC_SCRATCH_BYTES) return MOE_ERR_SCRATCH_LIMIT;
+    hipStream_t hs = static_cast<hipStream_t>(stream);
+    void* ws = nullptr;
+    if (scratch_for_stream(hs, &ws) != hipSuccess) return MOE_ERR_HIP;
+    if (!ws) return MOE_ERR_INVALID_ARG;  // the stream is not on the current device
+    return layer_forward(a, ws, MOE_NOALLOC_SCRATCH_BYTES, hs);
 }
 
 moe_status moe_pack_weights(const void* src, void* dst, int64_t rows, int64_t cols, int32_t dtype, void* stream) {

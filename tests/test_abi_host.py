@@ -61,8 +61,33 @@ def test_struct_layout_matches_header(pkg, tmp_path):
 def test_version_and_status_strings(pkg):
     assert pkg.lib.moe_abi_version() == 1
     assert pkg.status_str(0) == "ok"
-    for s in range(1, 5):
-        assert pkg.status_str(s) and pkg.status_str(s) != "ok"
+    strs = [pkg.status_str(s) for s in range(1, 6)]
+    assert all(v and v != "ok" for v in strs) and len(set(strs)) == 5
+    assert pkg.status_str(pkg.MOE_ERR_SCRATCH_LIMIT).startswith("layer needs more workspace")
+
+
+def test_noalloc_scratch_size_matches_header(pkg):
+    text = open(HEADER).read()
+    m = re.search(r"#define MOE_NOALLOC_SCRATCH_BYTES \(\(size_t\)(\d+) << (\d+)\)", text)
+    assert m and int(m.group(1)) << int(m.group(2)) == pkg.MOE_NOALLOC_SCRATCH_BYTES
+    assert re.search(r"MOE_ERR_SCRATCH_LIMIT = (\d+)", text).group(1) == str(pkg.MOE_ERR_SCRATCH_LIMIT)
+
+
+def test_noalloc_rejects_before_touching_a_device(pkg):
+    """The no-allocation forward checks the struct, the shape and the scratch limit on the host first:
+    a prefill-size layer (173 MiB of workspace) is refused with MOE_ERR_SCRATCH_LIMIT."""
+    big = pkg.make_dims(2048, 2048, 64, 1408, 6, shared=2, shared_ffn=1408, slots=48)
+    assert pkg.moe_workspace_bytes(big) > pkg.MOE_NOALLOC_SCRATCH_BYTES
+    a = pkg.moe_layer_args()
+    a.struct_size = ctypes.sizeof(pkg.moe_layer_args)
+    a.dims = big
+    assert pkg.lib.moe_layer_forward_noalloc(ctypes.byref(a), None) == pkg.MOE_ERR_SCRATCH_LIMIT
+    a.struct_size = 8
+    assert pkg.lib.moe_layer_forward_noalloc(ctypes.byref(a), None) == pkg.MOE_ERR_INVALID_ARG
+    a.struct_size = ctypes.sizeof(pkg.moe_layer_args)
+    a.dims = pkg.make_dims(32, 4096, 8, 14336, 9, slots=4)       # k > E
+    assert pkg.lib.moe_layer_forward_noalloc(ctypes.byref(a), None) == pkg.MOE_ERR_INVALID_ARG
+    assert pkg.lib.moe_layer_forward_noalloc(None, None) == pkg.MOE_ERR_INVALID_ARG
 
 
 GOOD = dict(tokens=32, hidden=4096, experts=8, ffn=14336, top_k=2, shared=0, shared_ffn=0, slots=4, dtype=1)
