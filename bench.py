@@ -16,7 +16,12 @@ Prints one JSON line on stdout:
   by the library around that kernel on the launch stream, against 8 TB/s (decode
   batches); for prefill-size batches (more than 64 tokens) its algorithmic
   FLOPs per launch / the same duration, against 2.5 PFLOP/s dense bf16;
-* cpu_baseline: the CPU oracle timed on this host on the same workload.
+* cpu_baseline: the CPU oracle timed on this host on the same workload;
+* workloads: the same measurement (step time, tokens/s, dominant-kernel and
+  whole-layer rooflines, stage breakdown, a shorter CPU-oracle sample) for every
+  other config -- the tiny fp32 layer, the shared+routed decode batch, the
+  prefill chunk (MFMA utilisation), one layer call of the stage-structured
+  trace and the Qwen3-MoE-like decode batch -- unless --only is given.
 """
 from __future__ import annotations
 
@@ -98,7 +103,12 @@ def layer_roofline(alg, ms_per_step: float):
 
 
 def cpu_baseline(layer, seconds: float):
-    """The CPU oracle (as it stands) on the same layer: whole batches until `seconds` have passed."""
+    """The CPU oracle (as it stands) on the same layer: whole batches until `seconds` have passed.
+
+    Two more legs, on at most 32 tokens of the batch (routing and repacking still
+    cover the whole batch): one thread, and the full layer with the offloaded
+    experts too."""
+    import numpy as np
     import oracle
     reps = 0
     t0 = time.perf_counter()
@@ -110,30 +120,34 @@ def cpu_baseline(layer, seconds: float):
             break
     toks = reps * layer.cfg.tokens
     n = oracle.threads()
-    # one batch on one thread as well (the oracle's results do not depend on the thread count)
+    T = layer.cfg.tokens
+    sample = None if T <= 32 else np.arange(32)
+    ns = T if sample is None else sample.size
+    # the sample on one thread (the oracle's results do not depend on the thread count)
     oracle.set_threads(1)
     t1 = time.perf_counter()
-    oracle.layer_forward_synthetic(layer, offloaded=False)
+    oracle.layer_forward_synthetic(layer, offloaded=False, sample=sample)
     el1 = time.perf_counter() - t1
     oracle.set_threads(n)
-    # the full layer as well: every pair, resident or offloaded (about a tenth of the time above),
-    # after one untimed call that first touches the offloaded experts' weights
-    oracle.layer_forward_synthetic(layer, offloaded=True)
+    # the full layer: every pair of the sample, resident or offloaded, after one untimed
+    # call that first touches the offloaded experts' weights
+    oracle.layer_forward_synthetic(layer, offloaded=True, sample=sample)
     full_reps = 0
     t2 = time.perf_counter()
     while True:
-        oracle.layer_forward_synthetic(layer, offloaded=True)
+        oracle.layer_forward_synthetic(layer, offloaded=True, sample=sample)
         full_reps += 1
         el2 = time.perf_counter() - t2
         if el2 >= seconds / 10:
             break
+    what = "tokens" if sample is None else f"of the first {ns} tokens (FFN; routing and repack over all {T})"
     return {"value": toks / el, "unit": "tokens/s", "cores": n, "kind": "oracle",
-            "sample": f"{reps} full batch(es) of {layer.cfg.tokens} tokens of the same layer (resident experts + "
+            "sample": f"{reps} full batch(es) of {T} tokens of the same layer (resident experts + "
                       f"router + repack, fp64 C with OpenMP), {el:.1f} s",
-            "single_thread": {"value": layer.cfg.tokens / el1, "unit": "tokens/s",
-                              "sample": f"1 batch of {layer.cfg.tokens} tokens, {el1:.1f} s"},
-            "full_layer": {"value": full_reps * layer.cfg.tokens / el2, "unit": "tokens/s",
-                           "sample": f"{full_reps} batch(es) with the offloaded experts too, {el2:.1f} s"},
+            "single_thread": {"value": ns / el1, "unit": "tokens/s",
+                              "sample": f"1 batch {what} on one thread, {el1:.1f} s"},
+            "full_layer": {"value": full_reps * ns / el2, "unit": "tokens/s",
+                           "sample": f"{full_reps} batch(es) {what} with the offloaded experts too, {el2:.1f} s"},
             **host_cpu_info()}
 
 
@@ -298,15 +312,235 @@ def trace_timings(seed: int, lags, detect: bool = False, persistence: float = 0.
     return out
 
 
+# the configs measured besides the primary one in a default run (each with its own
+# roofline and a bounded CPU-oracle sample): the tiny fp32 layer, the shared+routed
+# decode batch, the prefill chunk, one layer call of the stage-structured trace, and
+# the Qwen3-MoE-like decode batch
+OTHER_WORKLOADS = ["c1_tiny_f32", "c3_shared_decode", "c4_prefill", "c5_stage_trace", "c6_qwen3_decode"]
+
+
+def measure_workload(name, cfg, args, steps: int, warmup: int, cpu_seconds: float, primary: bool,
+                     read_probe_gbps=None):
+    """Times `steps` fused layer forwards of one workload (after `warmup` untimed ones) and
+    returns its measurement: step time, tokens/s, the dominant kernel's roofline, the whole
+    layer's roofline, the per-stage breakdown and (unless disabled) the CPU oracle's rate."""
+    import numpy as np
+    import torch
+
+    import paper_2608_21614_amd as moe
+    from paper_2608_21614_amd.device import DeviceLayer, to_host
+    from workloads import SyntheticLayer
+
+    log(f"[bench] generating {name} seed {args.seed}")
+    layer = SyntheticLayer(cfg, args.seed)
+    dev = DeviceLayer(layer)
+    copies = [(dev.w13, dev.w2)] + [(dev.w13.clone(), dev.w2.clone()) for _ in range(args.copies - 1)]
+    o = dev.alloc_outputs()
+    hip = moe.hip_runtime()
+    hip.hipEventCreateWithFlags.argtypes = [ctypes.POINTER(ctypes.c_void_p), ctypes.c_uint]
+    hip.hipEventElapsedTime.argtypes = [ctypes.POINTER(ctypes.c_float), ctypes.c_void_p, ctypes.c_void_p]
+    hip.hipEventDestroy.argtypes = [ctypes.c_void_p]
+    created = []
+
+    def new_event():
+        ev = ctypes.c_void_p()
+        assert hip.hipEventCreateWithFlags(ctypes.byref(ev), 0) == 0
+        created.append(ev.value)
+        return ev
+
+    nE = moe.MOE_STAGE_EVENTS
+    P1_BEFORE, P1_AFTER = 3, 4  # stage events around FFN phase 1
+    # every EVENT_EVERY-th timed step records the two events around the dominant
+    # kernel (each event record costs GPU time, about 2.5 us); a separate untimed
+    # pass records every stage boundary
+    timed_ev = [i for i in range(steps) if i % EVENT_EVERY == 0]
+    ev = {i: (ctypes.c_void_p * nE)(*[new_event().value if j in (P1_BEFORE, P1_AFTER) else None for j in range(nE)])
+          for i in timed_ev}
+    n_diag = min(steps, 50)
+    ev_all = [(ctypes.c_void_p * nE)(*[new_event().value for _ in range(nE)]) for _ in range(n_diag)]
+
+    def make_args(i, events=None):
+        w13, w2 = copies[i % len(copies)]
+        dev.w13, dev.w2 = w13, w2
+        a = dev.args(o)
+        if events is not None:
+            a.stage_events = ctypes.cast(events, ctypes.POINTER(ctypes.c_void_p))
+        return a
+
+    plain = [make_args(i) for i in range(len(copies))]
+    timed = [make_args(i, ev.get(i)) for i in range(steps)]
+    diag = [make_args(i, ev_all[i]) for i in range(n_diag)]
+    stream = torch.cuda.current_stream()
+
+    if primary and args.calib_copy_mib:
+        n = args.calib_copy_mib * (1 << 20) // 4
+        src = torch.ones(n, dtype=torch.float32, device="cuda")
+        dst = torch.empty_like(src)
+        torch.cuda.synchronize()
+        dst.copy_(src)
+        torch.cuda.synchronize()
+        log(f"[bench] calibration copy of {args.calib_copy_mib} MiB done")
+        del src, dst
+
+    for i in range(warmup):
+        moe.moe_layer_forward(plain[i % len(plain)], dev.ws, stream)
+    torch.cuda.synchronize()
+    log(f"[bench] {name}: warmup {warmup} done; timing {steps} steps")
+    t0 = time.perf_counter()
+    for i in range(steps):
+        moe.moe_layer_forward(timed[i], dev.ws, stream)
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+
+    f = ctypes.c_float()
+    p1_ms = np.zeros(len(timed_ev))
+    for n, i in enumerate(timed_ev):
+        assert hip.hipEventElapsedTime(ctypes.byref(f), ev[i][P1_BEFORE], ev[i][P1_AFTER]) == 0
+        p1_ms[n] = f.value
+
+    # untimed diagnostics: every stage boundary instrumented, and steps with no events at all
+    for i in range(n_diag):
+        moe.moe_layer_forward(diag[i], dev.ws, stream)
+    torch.cuda.synchronize()
+    stage_ms = np.zeros((n_diag, nE - 1))
+    for i in range(n_diag):
+        for j in range(nE - 1):
+            assert hip.hipEventElapsedTime(ctypes.byref(f), ev_all[i][j], ev_all[i][j + 1]) == 0
+            stage_ms[i, j] = f.value
+    stage_us = {n: float(stage_ms[:, j].mean() * 1e3) for j, n in enumerate(STAGES)}
+    step_us = stage_ms.sum(axis=1) * 1e3       # per instrumented step: first to last stage event
+    step_pct = {"p10": float(np.percentile(step_us, 10)), "median": float(np.median(step_us)),
+                "p90": float(np.percentile(step_us, 90)), "steps": int(n_diag)}
+    t1 = time.perf_counter()
+    for i in range(steps):
+        moe.moe_layer_forward(plain[i % len(plain)], dev.ws, stream)
+    torch.cuda.synchronize()
+    ms_no_events = (time.perf_counter() - t1) * 1e3 / steps
+
+    ms_graph = None
+    if primary:
+        # the same calls replayed from a HIP graph: one capture of one call per weight copy
+        side = torch.cuda.Stream()
+        side.wait_stream(stream)
+        with torch.cuda.stream(side):
+            for a in plain:
+                moe.moe_layer_forward(a, dev.ws)
+        stream.wait_stream(side)
+        torch.cuda.synchronize()
+        graph = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(graph):
+            for a in plain:
+                moe.moe_layer_forward(a, dev.ws)
+        reps = max(1, steps // len(plain))
+        graph.replay()
+        torch.cuda.synchronize()
+        t2 = time.perf_counter()
+        for _ in range(reps):
+            graph.replay()
+        torch.cuda.synchronize()
+        ms_graph = (time.perf_counter() - t2) * 1e3 / (reps * len(plain))
+        del graph
+
+    if read_probe_gbps is None:
+        # streaming-read reference of this GPU: one pass of 16-byte loads over 4 GiB
+        probe_src = torch.empty(1 << 30, dtype=torch.float32, device="cuda")
+        probe_sink = torch.zeros(1, dtype=torch.int32, device="cuda")
+        pe0, pe1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        for _ in range(2):
+            moe.moe_read_probe(probe_src, probe_sink, stream=stream)
+        pe0.record(stream)
+        for _ in range(10):
+            moe.moe_read_probe(probe_src, probe_sink, stream=stream)
+        pe1.record(stream)
+        torch.cuda.synchronize()
+        read_probe_gbps = 10 * probe_src.numel() * 4 / (pe0.elapsed_time(pe1) * 1e-3) / 1e9
+        del probe_src, probe_sink
+
+    counts = to_host(o["counts"])
+    resident = (layer.expert_slot >= 0) & (layer.expert_slot < dev.slots)
+    alg = algorithmic_bytes(cfg, counts, resident)
+    ms_per_step = wall * 1e3 / steps
+    tokens_per_s = cfg.tokens / (ms_per_step * 1e-3)
+    p1_us = float(p1_ms.mean() * 1e3)
+    p1_pct = {"p10": float(np.percentile(p1_ms, 10) * 1e3), "median": float(np.median(p1_ms) * 1e3),
+              "p90": float(np.percentile(p1_ms, 90) * 1e3)}
+    p1_s = p1_us * 1e-6
+    traffic = read_traffic(name)
+    if cfg.tokens > 64:
+        # prefill-size batches run the tiled MFMA kernels, at the ridge: FLOP rate
+        # against the dense bf16 matrix-core peak, and the HBM fraction beside it
+        achieved = alg["phase1_flops"] / p1_s / 1e12
+        roofline = {"kernel": "k_ffn_tiled (phase 1: gate/up projections + SwiGLU)", "bound": "mfma",
+                    "achieved": achieved, "peak": MFMA_BF16_PEAK_TFLOPS, "unit": "TFLOP/s",
+                    "frac": achieved / MFMA_BF16_PEAK_TFLOPS, "traffic": traffic,
+                    "algorithmic_flops_per_launch": alg["phase1_flops"],
+                    "algorithmic_bytes_per_launch": alg["phase1_bytes"],
+                    "hbm_frac_algorithmic": alg["phase1_bytes"] / p1_s / 1e9 / HBM_PEAK_GBPS, "mean_launch_us": p1_us,
+                    "launch_us": p1_pct, "launches_timed": len(timed_ev)}
+    else:
+        achieved = alg["phase1_bytes"] / p1_s / 1e9
+        roofline = {"kernel": "k_ffn_stream (phase 1: gate/up projections + SwiGLU)", "bound": "hbm",
+                    "achieved": achieved, "peak": HBM_PEAK_GBPS, "unit": "GB/s", "frac": achieved / HBM_PEAK_GBPS,
+                    "read_probe_GBps": read_probe_gbps, "frac_of_read_probe": achieved / read_probe_gbps,
+                    "traffic": traffic, "algorithmic_bytes_per_launch": alg["phase1_bytes"], "mean_launch_us": p1_us,
+                    "launch_us": p1_pct, "launches_timed": len(timed_ev)}
+    m = {
+        "workload": name,
+        "description": cfg.description,
+        "dtype": "bf16" if cfg.dtype == "bf16" else "f32",
+        "steps": steps,
+        "warmup": warmup,
+        "ms_per_step": ms_per_step,
+        "tokens_per_s": tokens_per_s,
+        "shape": {"tokens": cfg.tokens, "hidden": cfg.hidden, "experts": cfg.experts, "ffn": cfg.ffn,
+                  "top_k": cfg.top_k, "shared": cfg.shared, "shared_ffn": cfg.shared_ffn,
+                  "resident_slots": dev.slots, "active_resident_experts": alg["active"],
+                  "resident_pairs": alg["n_res"], "offloaded_pairs": alg["n_off"], "seed": args.seed,
+                  "weight_copies": len(copies)},
+        "hbm_gbps_expert_weights": alg["expert_weight_bytes"] / (ms_per_step * 1e-3) / 1e9,
+        "hbm_gbps_layer_algorithmic": alg["layer_bytes"] / (ms_per_step * 1e-3) / 1e9,
+        "mfma_tflops_layer_algorithmic": alg["flops"] / (ms_per_step * 1e-3) / 1e12,
+        "stages_us_instrumented": stage_us,
+        "step_us_instrumented": step_pct,
+        "ms_per_step_without_events": ms_no_events,
+        # whole layer against its roofline: the slower of moving its algorithmic bytes at
+        # the HBM peak and doing its algorithmic flops at the dense bf16 MFMA peak
+        "layer_roofline": layer_roofline(alg, ms_per_step),
+        "roofline": roofline,
+        "hbm_read_probe_GBps": read_probe_gbps,
+    }
+    if ms_graph is not None:
+        # the same calls replayed from a HIP graph (one graph launch per call instead of 5-6 kernel launches)
+        m["ms_per_step_graph"] = ms_graph
+    if primary and args.bookkeeping > 0:
+        m["bookkeeping"] = bookkeeping_timings(dev, args.bookkeeping)
+    if primary and args.hybrid > 0:
+        m["hybrid"] = hybrid_timings(layer, dev, args.hybrid, args.host_threads, args.hybrid_spare)
+    for e in created:
+        hip.hipEventDestroy(e)
+    del copies, dev, o, plain, timed, diag
+    torch.cuda.empty_cache()
+    if cpu_seconds > 0:
+        log(f"[bench] {name}: timing the CPU oracle ({cpu_seconds:.0f} s sample)")
+        m["cpu_baseline"] = cpu_baseline(layer, cpu_seconds)
+    return m
+
+
 def main() -> int:
     ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=200)
     ap.add_argument("--warmup", type=int, default=20)
-    ap.add_argument("--workload", default="c2_mixtral_decode")
+    ap.add_argument("--workload", default="c2_mixtral_decode",
+                    help="the primary workload, whose throughput is `value`")
+    ap.add_argument("--only", action="store_true",
+                    help="measure the primary workload only (default: the other configs follow, each as an "
+                         "entry of `workloads`)")
     ap.add_argument("--seed", type=int, default=0)
     ap.add_argument("--copies", type=int, default=4, help="rotated expert-weight copies")
     ap.add_argument("--cpu-seconds", type=float, default=10.0)
+    ap.add_argument("--other-cpu-seconds", type=float, default=3.0,
+                    help="CPU-oracle sample per other config (0: none)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--hybrid", type=int, default=0, metavar="N",
                     help="also time N hybrid layer calls (offloaded experts on the host, Section IV-D.2); "
@@ -336,12 +570,9 @@ def main() -> int:
                                    "MI355X; multi-GPU sharding is a design note, not built"}), flush=True)
         return 2
 
-    import numpy as np
     import torch
 
-    import paper_2608_21614_amd as moe
-    from paper_2608_21614_amd.device import DeviceLayer, to_host
-    from workloads import CONFIGS, TRACE, SyntheticLayer
+    from workloads import CONFIGS, TRACE
 
     # the stage-structured trace's layer shape is timed as one layer call (no stage bias)
     cfgs = dict(CONFIGS)
@@ -351,199 +582,44 @@ def main() -> int:
         return 2
     cfg = cfgs[args.workload]
     torch.cuda.set_device(0)
-    log(f"[bench] generating {args.workload} seed {args.seed}")
-    layer = SyntheticLayer(cfg, args.seed)
-    dev = DeviceLayer(layer)
-    copies = [(dev.w13, dev.w2)] + [(dev.w13.clone(), dev.w2.clone()) for _ in range(args.copies - 1)]
-    o = dev.alloc_outputs()
-    hip = moe.hip_runtime()
-    hip.hipEventCreateWithFlags.argtypes = [ctypes.POINTER(ctypes.c_void_p), ctypes.c_uint]
-    hip.hipEventElapsedTime.argtypes = [ctypes.POINTER(ctypes.c_float), ctypes.c_void_p, ctypes.c_void_p]
-    hip.hipEventSynchronize.argtypes = [ctypes.c_void_p]
-
-    def new_event():
-        ev = ctypes.c_void_p()
-        assert hip.hipEventCreateWithFlags(ctypes.byref(ev), 0) == 0
-        return ev
-
-    nE = moe.MOE_STAGE_EVENTS
-    P1_BEFORE, P1_AFTER = 3, 4  # stage events around FFN phase 1
-    # every EVENT_EVERY-th timed step records the two events around the dominant
-    # kernel (each event record costs GPU time, about 2.5 us); a separate untimed
-    # pass records every stage boundary
-    timed_ev = [i for i in range(args.steps) if i % EVENT_EVERY == 0]
-    ev = {i: (ctypes.c_void_p * nE)(*[new_event().value if j in (P1_BEFORE, P1_AFTER) else None for j in range(nE)])
-          for i in timed_ev}
-    n_diag = min(args.steps, 50)
-    ev_all = [(ctypes.c_void_p * nE)(*[new_event().value for _ in range(nE)]) for _ in range(n_diag)]
-
-    def make_args(i, events=None):
-        w13, w2 = copies[i % len(copies)]
-        dev.w13, dev.w2 = w13, w2
-        a = dev.args(o)
-        if events is not None:
-            a.stage_events = ctypes.cast(events, ctypes.POINTER(ctypes.c_void_p))
-        return a
-
-    plain = [make_args(i) for i in range(len(copies))]
-    timed = [make_args(i, ev.get(i)) for i in range(args.steps)]
-    diag = [make_args(i, ev_all[i]) for i in range(n_diag)]
-    stream = torch.cuda.current_stream()
-
-    if args.calib_copy_mib:
-        n = args.calib_copy_mib * (1 << 20) // 4
-        src = torch.ones(n, dtype=torch.float32, device="cuda")
-        dst = torch.empty_like(src)
-        torch.cuda.synchronize()
-        dst.copy_(src)
-        torch.cuda.synchronize()
-        log(f"[bench] calibration copy of {args.calib_copy_mib} MiB done")
-        del src, dst
-
-    for i in range(args.warmup):
-        moe.moe_layer_forward(plain[i % len(plain)], dev.ws, stream)
-    torch.cuda.synchronize()
-    log(f"[bench] warmup {args.warmup} done; timing {args.steps} steps")
-    t0 = time.perf_counter()
-    for i in range(args.steps):
-        moe.moe_layer_forward(timed[i], dev.ws, stream)
-    torch.cuda.synchronize()
-    wall = time.perf_counter() - t0
-
-    f = ctypes.c_float()
-    p1_ms = np.zeros(len(timed_ev))
-    for n, i in enumerate(timed_ev):
-        assert hip.hipEventElapsedTime(ctypes.byref(f), ev[i][P1_BEFORE], ev[i][P1_AFTER]) == 0
-        p1_ms[n] = f.value
-
-    # untimed diagnostics: every stage boundary instrumented, and steps with no events at all
-    for i in range(n_diag):
-        moe.moe_layer_forward(diag[i], dev.ws, stream)
-    torch.cuda.synchronize()
-    stage_ms = np.zeros((n_diag, nE - 1))
-    for i in range(n_diag):
-        for j in range(nE - 1):
-            assert hip.hipEventElapsedTime(ctypes.byref(f), ev_all[i][j], ev_all[i][j + 1]) == 0
-            stage_ms[i, j] = f.value
-    stage_us = {n: float(stage_ms[:, j].mean() * 1e3) for j, n in enumerate(STAGES)}
-    step_us = stage_ms.sum(axis=1) * 1e3       # per instrumented step: first to last stage event
-    step_pct = {"p10": float(np.percentile(step_us, 10)), "median": float(np.median(step_us)),
-                "p90": float(np.percentile(step_us, 90)), "steps": int(n_diag)}
-    t1 = time.perf_counter()
-    for i in range(args.steps):
-        moe.moe_layer_forward(plain[i % len(plain)], dev.ws, stream)
-    torch.cuda.synchronize()
-    ms_no_events = (time.perf_counter() - t1) * 1e3 / args.steps
-
-    # the same calls replayed from a HIP graph: one capture of one call per weight copy
-    side = torch.cuda.Stream()
-    side.wait_stream(stream)
-    with torch.cuda.stream(side):
-        for a in plain:
-            moe.moe_layer_forward(a, dev.ws)
-    stream.wait_stream(side)
-    torch.cuda.synchronize()
-    graph = torch.cuda.CUDAGraph()
-    with torch.cuda.graph(graph):
-        for a in plain:
-            moe.moe_layer_forward(a, dev.ws)
-    reps = max(1, args.steps // len(plain))
-    graph.replay()
-    torch.cuda.synchronize()
-    t2 = time.perf_counter()
-    for _ in range(reps):
-        graph.replay()
-    torch.cuda.synchronize()
-    ms_graph = (time.perf_counter() - t2) * 1e3 / (reps * len(plain))
-    del graph
-
-    # streaming-read reference of this GPU: one pass of 16-byte loads over 4 GiB
-    probe_src = torch.empty(1 << 30, dtype=torch.float32, device="cuda")
-    probe_sink = torch.zeros(1, dtype=torch.int32, device="cuda")
-    pe0, pe1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-    for _ in range(2):
-        moe.moe_read_probe(probe_src, probe_sink, stream=stream)
-    pe0.record(stream)
-    for _ in range(10):
-        moe.moe_read_probe(probe_src, probe_sink, stream=stream)
-    pe1.record(stream)
-    torch.cuda.synchronize()
-    read_probe_gbps = 10 * probe_src.numel() * 4 / (pe0.elapsed_time(pe1) * 1e-3) / 1e9
-    del probe_src, probe_sink
-
-    counts = to_host(o["counts"])
-    resident = (layer.expert_slot >= 0) & (layer.expert_slot < dev.slots)
-    alg = algorithmic_bytes(cfg, counts, resident)
-    ms_per_step = wall * 1e3 / args.steps
-    tokens_per_s = cfg.tokens / (ms_per_step * 1e-3)
-    p1_us = float(p1_ms.mean() * 1e3)
-    p1_pct = {"p10": float(np.percentile(p1_ms, 10) * 1e3), "median": float(np.median(p1_ms) * 1e3),
-              "p90": float(np.percentile(p1_ms, 90) * 1e3)}
-    p1_s = p1_us * 1e-6
-    traffic = read_traffic(args.workload)
-    if cfg.tokens > 64:
-        # prefill-size batches run the tiled MFMA kernels, at the ridge: FLOP rate
-        # against the dense bf16 matrix-core peak
-        achieved = alg["phase1_flops"] / p1_s / 1e12
-        roofline = {"kernel": "k_ffn_tiled (phase 1: gate/up projections + SwiGLU)", "bound": "mfma",
-                    "achieved": achieved, "peak": MFMA_BF16_PEAK_TFLOPS, "unit": "TFLOP/s",
-                    "frac": achieved / MFMA_BF16_PEAK_TFLOPS, "traffic": traffic,
-                    "algorithmic_flops_per_launch": alg["phase1_flops"],
-                    "algorithmic_bytes_per_launch": alg["phase1_bytes"],
-                    "hbm_frac_algorithmic": alg["phase1_bytes"] / p1_s / 1e9 / HBM_PEAK_GBPS, "mean_launch_us": p1_us,
-                    "launch_us": p1_pct, "launches_timed": len(timed_ev)}
-    else:
-        achieved = alg["phase1_bytes"] / p1_s / 1e9
-        roofline = {"kernel": "k_ffn_stream (phase 1: gate/up projections + SwiGLU)", "bound": "hbm",
-                    "achieved": achieved, "peak": HBM_PEAK_GBPS, "unit": "GB/s", "frac": achieved / HBM_PEAK_GBPS,
-                    "read_probe_GBps": read_probe_gbps, "frac_of_read_probe": achieved / read_probe_gbps,
-                    "traffic": traffic, "algorithmic_bytes_per_launch": alg["phase1_bytes"], "mean_launch_us": p1_us,
-                    "launch_us": p1_pct, "launches_timed": len(timed_ev)}
+    cpu_s = 0.0 if args.no_cpu_baseline else args.cpu_seconds
+    m = measure_workload(args.workload, cfg, args, args.steps, args.warmup, cpu_s, primary=True)
     result = {
         "metric": METRIC,
-        "value": tokens_per_s,
+        "value": m["tokens_per_s"],
         "unit": "tokens/s",
         "n_gpus": 1,
         "steps": args.steps,
         "warmup": args.warmup,
-        "ms_per_step": ms_per_step,
+        "ms_per_step": m["ms_per_step"],
         "higher_is_better": True,
         "scaling": "weak",
         "vs_baseline": None,
-        "dtype": "bf16" if cfg.dtype == "bf16" else "f32",
+        "dtype": m["dtype"],
         "data": f"synthetic (seeded: x ~ N(0,1), weights ~ N(0,0.02^2), {cfg.dtype})",
-        "config": {"workload": args.workload, "description": cfg.description, "tokens": cfg.tokens,
-                   "hidden": cfg.hidden, "experts": cfg.experts, "ffn": cfg.ffn, "top_k": cfg.top_k,
-                   "shared": cfg.shared, "shared_ffn": cfg.shared_ffn, "resident_slots": dev.slots,
-                   "active_resident_experts": alg["active"], "resident_pairs": alg["n_res"],
-                   "offloaded_pairs": alg["n_off"], "seed": args.seed, "weight_copies": len(copies),
-                   "parallelism": "1 GPU"},
-        "hbm_gbps_expert_weights": alg["expert_weight_bytes"] / (ms_per_step * 1e-3) / 1e9,
-        "hbm_gbps_layer_algorithmic": alg["layer_bytes"] / (ms_per_step * 1e-3) / 1e9,
-        "stages_us_instrumented": stage_us,
-        "step_us_instrumented": step_pct,
-        "ms_per_step_without_events": ms_no_events,
-        # the same calls replayed from a HIP graph (one graph launch per call instead of 5-6 kernel launches)
-        "ms_per_step_graph": ms_graph,
-        "hbm_read_probe_GBps": read_probe_gbps,
-        "mfma_tflops_layer_algorithmic": alg["flops"] / (ms_per_step * 1e-3) / 1e12,
-        # whole layer against its roofline: the slower of moving its algorithmic bytes at
-        # the HBM peak and doing its algorithmic flops at the dense bf16 MFMA peak
-        "layer_roofline": layer_roofline(alg, ms_per_step),
-        "roofline": roofline,
+        "config": {"workload": args.workload, "description": cfg.description, **m["shape"], "parallelism": "1 GPU"},
     }
-    if args.bookkeeping > 0:
-        result["bookkeeping"] = bookkeeping_timings(dev, args.bookkeeping)
-    if args.hybrid > 0:
-        result["hybrid"] = hybrid_timings(layer, dev, args.hybrid, args.host_threads, args.hybrid_spare)
+    for key in ("hbm_gbps_expert_weights", "hbm_gbps_layer_algorithmic", "stages_us_instrumented",
+                "step_us_instrumented", "ms_per_step_without_events", "ms_per_step_graph", "hbm_read_probe_GBps",
+                "mfma_tflops_layer_algorithmic", "layer_roofline", "roofline", "bookkeeping", "hybrid"):
+        if key in m:
+            result[key] = m[key]
+    if not args.only:
+        # every other config, one after another in the same process: same step count,
+        # same weight rotation, a shorter CPU-oracle sample each
+        other_cpu = 0.0 if args.no_cpu_baseline else args.other_cpu_seconds
+        result["workloads"] = {}
+        for name in OTHER_WORKLOADS:
+            if name == args.workload:
+                continue
+            result["workloads"][name] = measure_workload(name, cfgs[name], args, args.steps, args.warmup, other_cpu,
+                                                         primary=False, read_probe_gbps=m["hbm_read_probe_GBps"])
     if args.trace:
-        del copies, dev
         torch.cuda.empty_cache()
         result["trace"] = trace_timings(args.seed, [int(v) for v in args.trace.split(",")], args.detect,
                                         args.trace_persistence)
-    if not args.no_cpu_baseline:
-        log("[bench] timing the CPU oracle")
-        result["cpu_baseline"] = cpu_baseline(layer, args.cpu_seconds)
+    if "cpu_baseline" in m:
+        result["cpu_baseline"] = m["cpu_baseline"]
     print(json.dumps(result), flush=True)
     return 0
 
