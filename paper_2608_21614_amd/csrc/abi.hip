@@ -50,7 +50,7 @@ Shape shape_of(const moe_dims* d) {
 
 // Workspace layout (256-byte aligned regions).
 struct Layout {
-    size_t logits, idx, w, counts, seg, nres, perm, inv, part, act, y, total;
+    size_t logits, idx, w, counts, seg, nres, perm, inv, part, act, xg, meta, y, total;
     int ks, Fa;
     long long rows;
 };
@@ -78,8 +78,10 @@ Layout layout_of(const Shape& s) {
     L.perm = take(T * k * 4);
     L.inv = take(T * k * 4);
     L.part = take((size_t)saem::router_slices(s) * 64 * E * 4);
-    L.act = take((size_t)L.rows * L.Fa * (s.bf16 ? 2 : 4));
-    L.y = take((size_t)L.ks * L.rows * H * 4);
+    L.act = take((size_t)saem::ffn_act_rows(s) * L.Fa * (s.bf16 ? 2 : 4));
+    L.xg = take((size_t)saem::ffn_gather_rows(s) * H * 2);
+    L.meta = take(saem::ffn_tile_meta_bytes(s));
+    L.y = take(saem::ffn_y_bytes(s));
     L.total = off;
     return L;
 }
@@ -188,13 +190,20 @@ moe_status moe_grouped_ffn(const moe_dims* dims, const void* x, const int32_t* p
     a.x = x; a.perm = perm; a.counts = counts; a.seg_start = seg_start; a.expert_slot = expert_slot;
     a.w13 = w13; a.w2 = w2; a.ws13 = ws13; a.ws2 = ws2;
     a.act = at<char>(ws, L.act);
+    a.xg = at<char>(ws, L.xg);
+    a.tmeta = at<int32_t>(ws, L.meta);
     a.Fa = L.Fa;
     a.ks = L.ks;
     a.y_ks_stride = L.rows * (long long)s.H;
-    a.y = (L.ks == 1) ? y : at<float>(ws, L.y);
-    hipError_t e = saem::launch_grouped_ffn(s, a, hs);
-    if (e == hipSuccess && L.ks > 1)
-        e = saem::launch_reduce_splits(s, counts, expert_slot, a.y, L.ks, a.y_ks_stride, y, hs);
+    // the expert outputs go straight to y unless they are split-K partial sums or bf16 rows,
+    // which are added (widened) into y afterwards, resident and shared rows only
+    const bool y16 = saem::ffn_y_bf16(s);
+    a.y = (L.ks == 1 && !y16) ? y : at<float>(ws, L.y);
+    a.y16 = y16 ? at<char>(ws, L.y) : nullptr;
+    hipError_t e = saem::launch_gather_tokens(s, a, hs);
+    if (e == hipSuccess) e = saem::launch_grouped_ffn(s, a, hs);
+    if (e == hipSuccess && (L.ks > 1 || y16))
+        e = saem::launch_reduce_splits(s, counts, expert_slot, y16 ? a.y16 : a.y, y16, L.ks, a.y_ks_stride, y, hs);
     return hip_status(e);
 }
 
@@ -210,8 +219,8 @@ moe_status moe_combine(const moe_dims* dims, const int32_t* topk_idx, const floa
         return MOE_ERR_INVALID_ARG;
     if (y_off && !ok_ptr4(n_res)) return MOE_ERR_INVALID_ARG;
     const Shape s = shape_of(dims);
-    return hip_status(saem::launch_combine(s, topk_idx, topk_w, inv_perm, expert_slot, y, 1, 0, y_off, n_res, out,
-                                           out_dtype == MOE_BF16, static_cast<hipStream_t>(stream)));
+    return hip_status(saem::launch_combine(s, topk_idx, topk_w, inv_perm, expert_slot, y, false, 1, 0, y_off, n_res,
+                                           out, out_dtype == MOE_BF16, static_cast<hipStream_t>(stream)));
 }
 
 // The fused forward on a given workspace; moe_layer_forward and moe_layer_forward_noalloc
@@ -266,9 +275,6 @@ static moe_status layer_forward(const moe_layer_args* a, void* ws, size_t ws_byt
         return hip_status(e);
     }
     const bool fold_pack = saem::ffn_packs_offloaded(s);
-    if (e == hipSuccess)
-        e = mark(fold_pack ? hipSuccess
-                           : saem::launch_offload_pack(s, a->x, w, perm, nres, a->off_rows, a->off_w, hs), 3);
     saem::FfnArgs f;
     if (fold_pack) {
         f.topk_w = w;
@@ -279,13 +285,23 @@ static moe_status layer_forward(const moe_layer_args* a, void* ws, size_t ws_byt
     f.x = a->x; f.perm = perm; f.counts = counts; f.seg_start = seg; f.expert_slot = a->expert_slot;
     f.w13 = a->w13; f.w2 = a->w2; f.ws13 = a->ws13; f.ws2 = a->ws2;
     f.act = at<char>(ws, L.act);
+    f.xg = at<char>(ws, L.xg);
+    f.tmeta = at<int32_t>(ws, L.meta);
     f.Fa = L.Fa;
+    const bool y16 = saem::ffn_y_bf16(s);
     f.y = at<float>(ws, L.y);
+    f.y16 = y16 ? at<char>(ws, L.y) : nullptr;
     f.ks = L.ks;
     f.y_ks_stride = L.rows * (long long)s.H;
+    // the token gather of the bf16 prefill path (with the offloaded-row pack), or the
+    // standalone pack of the fp32 prefill path; at decode the pack is in FFN phase 1
+    if (e == hipSuccess)
+        e = mark(fold_pack ? saem::launch_gather_tokens(s, f, hs)
+                           : saem::launch_offload_pack(s, a->x, w, perm, nres, a->off_rows, a->off_w, hs), 3);
     if (e == hipSuccess) e = mark(saem::launch_grouped_ffn(s, f, hs, ev[4]), 5);
     if (e == hipSuccess)
-        e = mark(saem::launch_combine(s, idx, w, inv, a->expert_slot, f.y, L.ks, f.y_ks_stride, nullptr, nullptr,
+        e = mark(saem::launch_combine(s, idx, w, inv, a->expert_slot, at<char>(ws, L.y), y16, L.ks, f.y_ks_stride,
+                                      nullptr, nullptr,
                                       a->out, a->out_dtype == MOE_BF16, hs), 6);
     return hip_status(e);
 }

@@ -36,12 +36,20 @@ __device__ __forceinline__ f32x4 sum_chunks(const float* __restrict__ y, int ks,
 // then the sums run in the fixed order above.  KS >= ks is the compile-time
 // bound on the K chunks; above two chunks the loads go one contribution at a
 // time (all of its chunks together), which keeps the registers in bounds.
-template <bool kOutBf16, int KS>
+template <bool kOutBf16, int KS, bool kYBf16 = false>
 __global__ void __launch_bounds__(256)
     k_combine(int T, int H, int E, int k, int S, int slots, const int32_t* __restrict__ topk_idx,
               const float* __restrict__ topk_w, const int32_t* __restrict__ inv_perm,
-              const int32_t* __restrict__ expert_slot, const float* __restrict__ y, int ks, long long stride,
+              const int32_t* __restrict__ expert_slot, const void* __restrict__ y_any, int ks, long long stride,
               const float* __restrict__ y_off, const int32_t* __restrict__ n_res_p, void* __restrict__ out) {
+    static_assert(!kYBf16 || KS == 1, "bf16 expert outputs come in one chunk");
+    const float* __restrict__ y = static_cast<const float*>(y_any);
+    const uint16_t* __restrict__ y16 = static_cast<const uint16_t*>(y_any);
+    // four consecutive outputs of row r at column h of the expert outputs
+    auto yrow4 = [&](size_t off) -> f32x4 {
+        if constexpr (kYBf16) return bf16x4_to_f32(*reinterpret_cast<const u32x2*>(y16 + off));
+        else return *reinterpret_cast<const f32x4*>(y + off);
+    };
     constexpr int kK = 8, kS = 8;  // bounds on k and S (the ABI checks both)
     const int t = blockIdx.x;
     const int h = (blockIdx.y * 256 + threadIdx.x) * 4;
@@ -81,12 +89,19 @@ __global__ void __launch_bounds__(256)
 #pragma unroll
         for (int j = 0; j < kK; ++j) {
             const size_t off = (size_t)(src[j] ? p[j] : 0) * H + h;
-            const float* base = (src[j] == 2) ? y_off + (off - (size_t)nres * H) : y + off;
+            if constexpr (kYBf16) {
+                // one chunk; a row from y_off (fp32) or from the bf16 expert outputs
+                const f32x4 l = (src[j] == 2) ? *reinterpret_cast<const f32x4*>(y_off + (off - (size_t)nres * H))
+                                              : yrow4(off);
+                v[j][0] = src[j] ? l : zero;
+            } else {
+                const float* base = (src[j] == 2) ? y_off + (off - (size_t)nres * H) : y + off;
 #pragma unroll
-            for (int c = 0; c < KS; ++c) {
-                const bool use = src[j] == 1 ? c < ks : (src[j] == 2 && c == 0);
-                const f32x4 l = *reinterpret_cast<const f32x4*>(base + (use ? c * stride : 0));
-                v[j][c] = use ? l : zero;
+                for (int c = 0; c < KS; ++c) {
+                    const bool use = src[j] == 1 ? c < ks : (src[j] == 2 && c == 0);
+                    const f32x4 l = *reinterpret_cast<const f32x4*>(base + (use ? c * stride : 0));
+                    v[j][c] = use ? l : zero;
+                }
             }
         }
 #pragma unroll
@@ -95,7 +110,7 @@ __global__ void __launch_bounds__(256)
 #pragma unroll
             for (int c = 0; c < KS; ++c) {
                 const bool use = s2 < S && c < ks;
-                const f32x4 l = *reinterpret_cast<const f32x4*>(y + off + (use ? c * stride : 0));
+                const f32x4 l = yrow4(off + (use ? c * stride : 0));
                 vs[s2][c] = use ? l : zero;
             }
         }
@@ -138,14 +153,15 @@ __global__ void k_stage_accumulate(int E, const int32_t* __restrict__ counts, in
 
 template <bool kOutBf16>
 hipError_t launch_combine_ks(dim3 grid, const Shape& s, const int32_t* topk_idx, const float* topk_w,
-                             const int32_t* inv_perm, const int32_t* expert_slot, const float* y, int ks,
+                             const int32_t* inv_perm, const int32_t* expert_slot, const void* y, bool y_bf16, int ks,
                              long long stride, const float* y_off, const int32_t* n_res, void* out, hipStream_t st) {
-#define SAEM_COMBINE(KS)                                                                                            \
-    hipLaunchKernelGGL((k_combine<kOutBf16, KS>), grid, dim3(256), 0, st, s.T, s.H, s.E, s.k, s.S, s.slots,      \
+#define SAEM_COMBINE(KS, YB)                                                                                        \
+    hipLaunchKernelGGL((k_combine<kOutBf16, KS, YB>), grid, dim3(256), 0, st, s.T, s.H, s.E, s.k, s.S, s.slots,  \
                        topk_idx, topk_w, inv_perm, expert_slot, y, ks, stride, y_off, n_res, out)
-    if (ks <= 1) SAEM_COMBINE(1);
-    else if (ks <= 2) SAEM_COMBINE(2);
-    else SAEM_COMBINE(16);
+    if (y_bf16) SAEM_COMBINE(1, true);
+    else if (ks <= 1) SAEM_COMBINE(1, false);
+    else if (ks <= 2) SAEM_COMBINE(2, false);
+    else SAEM_COMBINE(16, false);
 #undef SAEM_COMBINE
     return hipGetLastError();
 }
@@ -153,15 +169,15 @@ hipError_t launch_combine_ks(dim3 grid, const Shape& s, const int32_t* topk_idx,
 }  // namespace
 
 hipError_t launch_combine(const Shape& s, const int32_t* topk_idx, const float* topk_w, const int32_t* inv_perm,
-                          const int32_t* expert_slot, const float* y, int ks, long long y_ks_stride,
+                          const int32_t* expert_slot, const void* y, bool y_bf16, int ks, long long y_ks_stride,
                           const float* y_off, const int32_t* n_res, void* out, bool out_bf16, hipStream_t st) {
     if (s.T == 0) return hipSuccess;
-    if (ks < 1 || ks > 16 || s.k > 8 || s.S > 8) return hipErrorInvalidValue;
+    if (ks < 1 || ks > 16 || s.k > 8 || s.S > 8 || (y_bf16 && ks != 1)) return hipErrorInvalidValue;
     const dim3 grid(s.T, (s.H + 1023) / 1024);
-    return out_bf16 ? launch_combine_ks<true>(grid, s, topk_idx, topk_w, inv_perm, expert_slot, y, ks, y_ks_stride,
-                                              y_off, n_res, out, st)
-                    : launch_combine_ks<false>(grid, s, topk_idx, topk_w, inv_perm, expert_slot, y, ks, y_ks_stride,
-                                               y_off, n_res, out, st);
+    return out_bf16 ? launch_combine_ks<true>(grid, s, topk_idx, topk_w, inv_perm, expert_slot, y, y_bf16, ks,
+                                              y_ks_stride, y_off, n_res, out, st)
+                    : launch_combine_ks<false>(grid, s, topk_idx, topk_w, inv_perm, expert_slot, y, y_bf16, ks,
+                                               y_ks_stride, y_off, n_res, out, st);
 }
 
 hipError_t launch_stage_accumulate(int E, const int32_t* counts, int64_t* log, hipStream_t st) {

@@ -9,6 +9,7 @@ namespace saem {
 // bf16 data are carried as raw 16-bit patterns; MFMA operands are 8 x bf16 per lane.
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef float f32x4 __attribute__((ext_vector_type(4)));
+typedef float f32x16 __attribute__((ext_vector_type(16)));
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
 
@@ -97,7 +98,15 @@ __device__ __forceinline__ f32x4 mma_frag(const Frag8<float>& a, const Frag8<flo
     return c;
 }
 
-__device__ __forceinline__ float silu(float z) { return z / (1.0f + __expf(-z)); }
+// silu(z) = z / (1 + e^-z), with the hardware reciprocal (about 1 ulp) instead of a
+// correctly rounded divide; z = -inf gives NaN, as the quotient does.
+__device__ __forceinline__ float silu(float z) { return z * __builtin_amdgcn_rcpf(1.0f + __expf(-z)); }
+
+// Four bf16 values (8 bytes) widened to fp32.
+__device__ __forceinline__ f32x4 bf16x4_to_f32(u32x2 v) {
+    return f32x4{__uint_as_float(v.x << 16), __uint_as_float(v.x & 0xffff0000u), __uint_as_float(v.y << 16),
+                 __uint_as_float(v.y & 0xffff0000u)};
+}
 
 __device__ __forceinline__ int lane_id() { return threadIdx.x & (kWave - 1); }
 

@@ -2,8 +2,8 @@
 // (SAEM Section IV-D.2: resident experts on the matrix cores; Section IV-E.1:
 // one batched execution per expert over its contiguous, repacked rows).
 //
-// Row space: packed rows [0, T*k) (resident experts first, see repack.hip),
-// then the rows of shared expert s at T*k + s*T + t.
+// Row space of the expert outputs: packed rows [0, T*k) (resident experts
+// first, see repack.hip), then the rows of shared expert s at T*k + s*T + t.
 //   phase 1: act[p, f] = silu(x[tok(p)] . W1[:,f]) * (x[tok(p)] . W3[:,f])
 //   phase 2: y[c][p, h] = sum over K chunk c of act[p, :] . W2[:,h]
 //
@@ -24,11 +24,11 @@
 //    splits K across workgroups into `ks` chunks whose partial sums the combine
 //    adds in fixed order.  SwiGLU is applied in the phase-1 epilogue, so the gate
 //    and up projections are never stored.
-//  * tiled   (bf16, T > 64, prefill): workgroup tiles of 128 weight rows x 128
-//    tokens (64 x 64 per wave); K runs in 64-wide slabs through one LDS buffer
-//    while the next slab is loaded into registers, so three workgroups fit on a
-//    CU; each phase-1 wave holds the gate and up rows of the same features so
-//    SwiGLU runs in registers.
+//  * tiled   (bf16, T > 64, prefill): one 256 x 256 output tile per workgroup
+//    (eight waves of 128 x 64 on MFMA 32x32x16), both operands read as 1 KB
+//    tile-layout blocks by direct global->LDS loads through a five-stage ring;
+//    a token gather first copies the resident groups' rows into that layout,
+//    and phase 1 writes the activations in it; the expert outputs are bf16.
 //  * f32     (fp32, T > 64): plain fp32 FMA, one output per thread.
 // All of them read counts and offsets from device memory: the grid is sized for
 // the worst case on the host and surplus workgroups exit at once.
@@ -62,6 +62,10 @@ struct Args {
     const int32_t* n_res;
     void* off_rows;
     float* off_w;
+    void* xg;         // bf16 prefill: gathered token rows in the tile layout
+    int32_t* tmeta;   // bf16 prefill: item tables of the tiled kernels
+    int tcap1;        // capacity of the phase-1 table
+    uint16_t* y16;    // bf16 prefill: expert outputs [rows][H] in bf16 (instead of y)
 };
 
 // off_rows[p - n_res] = x[perm[p] / k] and off_w[p - n_res] = topk_w[perm[p]] for the
@@ -379,27 +383,102 @@ __global__ void __launch_bounds__(256) k_ffn_stream(Args a) {
 // ---------------------------------------------------------------------------
 // tiled kernel (prefill)
 // ---------------------------------------------------------------------------
+//
+// One item = one 256 x 256 output tile of one group: 256 weight rows (phase 1:
+// 128 features, their gate and up rows; phase 2: 256 rows of W2) x 256 of the
+// group's rows.  Eight waves in 2 (rows) x 4 (tokens), each 128 rows x 64
+// tokens = 4 x 2 tiles of v_mfma_f32_32x32x16_bf16 (128 fp32 accumulators per
+// lane); a phase-1 wave holds the gate and the up rows of the same 64 features,
+// so SwiGLU runs in registers.  Wave w is (w % 2, w / 2), so an item whose
+// group ends within its first 128 rows still keeps one wave busy on each SIMD,
+// and a wave whose 64 tokens all lie past the group's end skips its MFMAs.
+//
+// Operands: both are read as 1 KB blocks of the MFMA tile layout (16 rows x 32
+// columns; lane l's 16 bytes are row l % 16, columns 8 (l / 16) .. + 7): the
+// weights as they are stored, the tokens from a copy that the token gather
+// (k_gather_tokens) makes of the resident groups' rows, and phase 2's from the
+// activations, which phase 1 writes in that layout.  A CU fills its LDS about
+// three times faster from such contiguous blocks than from loads that gather
+// 64 bytes from each of 16 row-major token rows.
+//
+// K runs in 32-wide slabs through a ring of kGStages LDS stages (32 KB each:
+// 16 weight blocks, 16 token blocks) filled by direct global->LDS loads: one
+// wave instruction moves one 1 KB block, lane l's 16 bytes landing at byte
+// 16 l, so every MFMA operand is one conflict-free 16-byte LDS read per lane.
+// The loads are issued as inline assembly and waited for by count (the
+// compiler cannot see their LDS writes, so it does not make every LDS read wait
+// for all of them): each wave issues exactly four per slab and no other
+// vector-memory instruction in the K loop, so "slab kt has landed" is "at most
+// 4 x (slabs issued after kt) loads outstanding", then a barrier.  The ring is
+// the kernel's only LDS: kGStages - 1 slabs (128 KB) stay in flight while one is
+// multiplied, which is what the load latency under this traffic asks for.
+//
+// Items come from a table the token gather writes (one scalar load per
+// workgroup); group g owns (weight tiles) x ceil(rows / 256) items, weight tile
+// major.  The XCDs get equal contiguous ranges of the real items (the hardware
+// deals workgroups to the 8 XCDs round-robin), so the 32 CUs of an XCD work on
+// neighbouring tiles of one group and share its weight and token panels in
+// their L2.
 
-constexpr int kTn = 128;         // tokens per tile
-constexpr int kTk = 64;          // K slab
-constexpr int kXPitch = kTk + 8;  // LDS row pitch of the token tile (bf16 elements)
+constexpr int kGM = 256;          // weight rows per item
+constexpr int kGN = 256;          // group rows (tokens) per item
+constexpr int kGStages = 5;       // LDS ring
+constexpr int kGStageBytes = 32 * 1024;
+constexpr int kGMaxGroups = 264;  // 256 routed + 8 shared
 
-// Active routed experts and the prefix of their kTn-token tile counts.
-__device__ int list_tiles(const Args& a, int* s_list, int* s_wsum, int* s_tpre, int nact) {
-    // s_tpre[g] = sum_{g' < g} ceil(count(g') / kTn); s_tpre[nact] = total
+// One item of the tiled kernels (a single 32-byte scalar load).
+struct __attribute__((aligned(32))) TileItem {
+    int32_t wsel;     // slot of the routed expert (>= 0), or -(s + 1) for shared expert s
+    int32_t count;    // rows of the group
+    int32_t rowbase;  // first row of the group in the packed row space (y)
+    int32_t Fg;       // expert width
+    int32_t xblk;     // first row block of the group's token rows in xg
+    int32_t ablk;     // first row block of the group's activations
+    int32_t wt;       // weight tile
+    int32_t n0;       // first group row of the tile
+};
+// Tile metadata: int32 header[8] (items of phase 1, of phase 2), then
+// TileItem phase1[cap1], phase2[cap2].
+
+typedef __attribute__((address_space(3))) uint8_t lds_u8;
+
+// One direct global -> LDS load of 16 bytes per lane: lane l's bytes from g land
+// at LDS byte address lds + 16 l (lds is wave-uniform, passed through M0).
+__device__ __forceinline__ void lds_load_1k(uint32_t lds, const void* g) {
+    asm volatile(
+        "s_mov_b32 m0, %0\n\t"
+        "s_nop 0\n\t"
+        "global_load_lds_dwordx4 %1, off"
+        :
+        : "s"(lds), "v"(g)
+        : "memory", "m0");
+}
+
+// Wait until at most N of this wave's vector-memory loads are outstanding and its
+// LDS accesses are done, then a workgroup barrier.  The memory clobber keeps
+// the compiler's LDS accesses on their side of it.
+template <int N>
+__device__ __forceinline__ void wait_then_barrier() {
+    asm volatile("s_waitcnt vmcnt(%0) lgkmcnt(0)\n\ts_barrier" : : "n"(N) : "memory");
+}
+
+__device__ __forceinline__ f32x16 mfma32x32x16(bf16x8 a, bf16x8 b, f32x16 c) {
+    return __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, b, c, 0, 0, 0);
+}
+
+// s_out[g] = sum_{g' < g} f(g') for g < n (n <= kGMaxGroups), s_out[n] = the total,
+// which is also returned; wave 0 scans, every thread of the workgroup must call.
+// *s_tot must not be read by any thread between its previous use and this call.
+template <typename Fn>
+__device__ int group_prefix(int n, int* s_out, int* s_tot, Fn f) {
     if (threadIdx.x < 64) {
         const int lane = threadIdx.x;
-        int v[4], sum = 0;
+        constexpr int PER = (kGMaxGroups + 63) / 64;
+        int v[PER], sum = 0;
 #pragma unroll
-        for (int i = 0; i < 4; ++i) {
-            const int gi = 4 * lane + i;
-            v[i] = 0;
-            if (gi < nact) {
-                const int e = s_list[gi];
-                int c = a.counts[e];
-                c = c < 0 ? 0 : c;
-                v[i] = (c + kTn - 1) / kTn;
-            }
+        for (int i = 0; i < PER; ++i) {
+            const int gi = PER * lane + i;
+            v[i] = gi < n ? f(gi) : 0;
             sum += v[i];
         }
         int inc = sum;
@@ -410,186 +489,319 @@ __device__ int list_tiles(const Args& a, int* s_list, int* s_wsum, int* s_tpre, 
         }
         int run = inc - sum;
 #pragma unroll
-        for (int i = 0; i < 4; ++i) {
-            const int gi = 4 * lane + i;
-            if (gi <= nact) s_tpre[gi] = run;
+        for (int i = 0; i < PER; ++i) {
+            const int gi = PER * lane + i;
+            if (gi < n) s_out[gi] = run;
             run += v[i];
         }
-        // the end entry: written above for nact < 256 (its run is then the total); with all
-        // 256 experts active it lies past the lanes' entries, so lane 63 writes it
         if (lane == 63) {
-            s_wsum[0] = inc;
-            s_tpre[nact] = inc;
+            s_out[n] = inc;
+            *s_tot = inc;
         }
     }
     __syncthreads();
-    return s_wsum[0];
+    return *s_tot;
 }
 
-// Workgroup tile: 128 weight rows x 128 tokens; phase 1 takes 64 features (their
-// 64 gate rows and 64 up rows), phase 2 128 rows of W2.  Four waves in 2 x 2,
-// each 64 rows x 64 tokens (16 MFMA 16x16x32 tiles, 64 fp32 accumulators per
-// lane); phase-1 waves hold the gate and up rows of the same 32 features so
-// SwiGLU runs in registers.  K runs in 64-wide slabs through one LDS buffer:
-// the weight slab is 16 blocks of 1 KB copied as they sit in the tile layout,
-// the token slab 128 gathered rows.  Consecutive tiles (same weight tile, next
-// token tile of the group) are placed on the same XCD so they share its L2.
-template <bool kDown>
-__global__ void __launch_bounds__(256, 3) k_ffn_tiled(Args a, int max_rtiles, int ntn_r, int ntn_s, int grid8) {
-    __shared__ int s_list[256];
-    __shared__ int s_wsum[4];
-    __shared__ int s_tpre[260];
-    __shared__ __attribute__((aligned(16))) uint16_t sW[16][512];
-    __shared__ __attribute__((aligned(16))) uint16_t sX[kTn][kXPitch];
+// Weight tiles of a group of width Fg: phase 1 covers 128 features per tile, phase 2 256 rows of W2.
+__device__ __forceinline__ int weight_tiles(const Args& a, int Fg, bool down) {
+    return down ? (a.H + kGM - 1) / kGM : (Fg + kGM / 2 - 1) / (kGM / 2);
+}
 
+// Writes both phases' item tables: the groups are the active resident routed
+// experts (s_list order, with their (segment start, count, slot) in s_info) and
+// then the S shared experts; s_bpre holds the routed groups' row-block prefix.
+__device__ void write_tile_items(const Args& a, int nact, const int4* s_info, const int* s_bpre, int rb_routed,
+                                 int* s_ipre, int* s_tot) {
+    const int ng = nact + a.S;
+    const int tb16 = (a.T + 15) / 16;
+    TileItem* tab = reinterpret_cast<TileItem*>(a.tmeta + 8);
+    for (int ph = 0; ph < 2; ++ph) {
+        const bool down = ph == 1;
+        const int total = group_prefix(ng, s_ipre, s_tot + ph, [&](int gi) {
+            const int rows = gi < nact ? max(s_info[gi].y, 0) : a.T;
+            const int Fg = gi < nact ? a.F : a.Fs;
+            return weight_tiles(a, Fg, down) * ((rows + kGN - 1) / kGN);
+        });
+        TileItem* out = tab + (down ? a.tcap1 : 0);
+        for (int i = threadIdx.x; i < total; i += blockDim.x) {
+            int lo = 0, hi = ng - 1;  // last group with s_ipre[g] <= i
+            while (lo < hi) {
+                const int mid = (lo + hi + 1) >> 1;
+                if (s_ipre[mid] <= i) lo = mid;
+                else hi = mid - 1;
+            }
+            TileItem it;
+            if (lo < nact) {
+                const int4 inf = s_info[lo];
+                const int P = a.T * a.k;
+                const int rb = min(max(inf.x, 0), P);
+                it.wsel = inf.z;
+                it.count = min(max(inf.y, 0), P - rb);
+                it.rowbase = rb;
+                it.Fg = a.F;
+                it.xblk = s_bpre[lo];
+                it.ablk = s_bpre[lo];
+            } else {
+                const int sh = lo - nact;
+                it.wsel = -(sh + 1);
+                it.count = a.T;
+                it.rowbase = a.T * a.k + sh * a.T;
+                it.Fg = a.Fs;
+                it.xblk = rb_routed;
+                it.ablk = rb_routed + sh * tb16;
+            }
+            const int ntt = (it.count + kGN - 1) / kGN;
+            const int local = i - s_ipre[lo];
+            it.wt = local / ntt;
+            it.n0 = (local % ntt) * kGN;
+            out[i] = it;
+        }
+        if (threadIdx.x == 0) a.tmeta[ph] = total;
+        __syncthreads();  // s_ipre is rewritten for the next phase
+    }
+}
+
+// The bf16 prefill operands in the MFMA tile layout (16-row x 32-column blocks of
+// 1 KB), so that every operand load of the tiled kernel is one contiguous 1 KB
+// block.  Row-block space (16 rows per block):
+//   xg: routed group gi (active list order) at blocks [bpre[gi], bpre[gi + 1]),
+//       its rows in packed order, the rows past the group zero; then, when there
+//       are shared experts, the batch's tokens in order at [RB, RB + ceil(T / 16)),
+//       RB = bpre[nact];
+//   act: the same for the routed groups; shared expert s at RB + s ceil(T / 16).
+// Block (rb, c) of a buffer with K columns starts at element (rb K / 32 + c) 512.
+// Workgroup 0 also writes the tiled kernels' item tables; the workgroups past
+// the row blocks pack the offloaded rows.
+__global__ void __launch_bounds__(256) k_gather_tokens(Args a, int blocks_max) {
+    __shared__ int s_list[256];
+    __shared__ int4 s_info[256];
+    __shared__ int s_wsum[8];
+    __shared__ int s_bpre[257];
+    __shared__ int s_ipre[kGMaxGroups + 1];
+    __shared__ int s_tok[16];
     const int pid = blockIdx.x;
-    if (!kDown && pid >= grid8) {  // workgroups past the items pack the offloaded rows (phase 1 only)
-        pack_offloaded(a, pid - grid8, gridDim.x - grid8, 2);
+    if (pid >= blocks_max) {
+        pack_offloaded(a, pid - blocks_max, gridDim.x - blocks_max, 2);
         return;
     }
-    const int nact = list_active(a, s_list, s_wsum);
-    const int total_rt = list_tiles(a, s_list, s_wsum, s_tpre, nact);
-    // XCD-aware order: workgroups are dealt to the 8 XCDs round-robin, so logical
-    // items pid/8, pid/8 + 1, ... of one XCD are consecutive in this numbering.
-    const int item = (pid % 8) * (grid8 / 8) + pid / 8;
-    Group g;
-    int mt_local, wn;
-    // inside a group, items run weight tile by weight tile and, for each, over
-    // all of the group's token tiles: the token tiles of one weight panel are
-    // consecutive on one XCD, so the panel is read from HBM about once
-    if (item < max_rtiles * ntn_r) {
-        const int gt = item / ntn_r;  // group gi owns items [ntn_r s_tpre[gi], ntn_r s_tpre[gi + 1])
-        if (gt >= total_rt) return;
-        int lo = 0, hi = nact - 1;  // last gi with s_tpre[gi] <= gt
-        while (lo < hi) {
-            const int mid = (lo + hi + 1) >> 1;
-            if (s_tpre[mid] <= gt) lo = mid;
-            else hi = mid - 1;
+    const int nact = list_active(a, s_list, s_wsum, s_info);
+    const int rb_routed =
+        group_prefix(nact, s_bpre, s_wsum + 4, [&](int gi) { return (max(s_info[gi].y, 0) + 15) / 16; });
+    if (pid == 0) write_tile_items(a, nact, s_info, s_bpre, rb_routed, s_ipre, s_wsum + 5);
+    if (threadIdx.x < 16) {
+        const int r = threadIdx.x;
+        int t = -1;
+        if (pid < rb_routed) {
+            int lo = 0, hi = nact - 1;
+            while (lo < hi) {
+                const int mid = (lo + hi + 1) >> 1;
+                if (s_bpre[mid] <= pid) lo = mid;
+                else hi = mid - 1;
+            }
+            const int4 inf = s_info[lo];
+            const Group g = routed_group_of(a, inf.x, inf.y, inf.z, 2);
+            t = group_token(a, g, 16 * (pid - s_bpre[lo]) + r);
+        } else {
+            const int n = 16 * (pid - rb_routed) + r;
+            t = (a.S > 0 && n < a.T) ? n : -1;
         }
-        g = routed_group(a, s_list[lo], 2);
-        const int tg = s_tpre[lo + 1] - s_tpre[lo];
-        const int local = item - ntn_r * s_tpre[lo];
-        wn = local / tg;
-        mt_local = local % tg;
-    } else {
-        const int i2 = item - max_rtiles * ntn_r;
-        const int tps = (a.T + kTn - 1) / kTn;
-        const int s = i2 / (tps * ntn_s);
-        if (s >= a.S) return;
-        g = shared_group(a, s, 2);
-        const int local = i2 % (tps * ntn_s);
-        wn = local / tps;
-        mt_local = local % tps;
+        s_tok[r] = t;
     }
-    const int n0 = mt_local * kTn;
-    if (n0 >= g.count) return;
+    __syncthreads();
+    if (pid >= rb_routed && (a.S == 0 || pid - rb_routed >= (a.T + 15) / 16)) return;
+    // 16-byte piece j of block c: row j % 16, columns 32 c + 8 (j / 16) .. + 7
+    const int nc = a.H / 32;
+    const uint16_t* x = static_cast<const uint16_t*>(a.x);
+    u32x4* dst = reinterpret_cast<u32x4*>(static_cast<uint16_t*>(a.xg) + (size_t)pid * nc * 512);
+    for (int idx = threadIdx.x; idx < nc * 64; idx += 256) {
+        const int c = idx >> 6, j = idx & 63;
+        const int t = s_tok[j & 15];
+        u32x4 v = {0u, 0u, 0u, 0u};
+        if (t >= 0) v = *reinterpret_cast<const u32x4*>(x + (size_t)t * a.H + 32 * c + 8 * (j >> 4));
+        dst[idx] = v;
+    }
+}
 
-    const int tid = threadIdx.x, wave = tid >> 6, lane = lane_id();
-    const int K = kDown ? g.Fg : a.H;
-    const int nst = K / 32;
-    const uint16_t* wbase = reinterpret_cast<const uint16_t*>(kDown ? g.w2 : g.w13);
-    const int wrow0 = wn * (kDown ? 128 : 64);  // first output row (phase 2) or feature (phase 1)
-    const int rows_total = kDown ? a.H : 2 * g.Fg;
+template <bool kDown>
+__global__ void __launch_bounds__(512, 1) k_ffn_tiled(Args a) {
+    __shared__ __attribute__((aligned(1024))) uint8_t sbuf[kGStages * kGStageBytes];
 
-    // the 8 row tiles of the weight slab: phase 1 gate f0/16 + 0..3, then up; phase 2 h0/16 + 0..7
-    int rt_of[8];
-#pragma unroll
-    for (int i = 0; i < 8; ++i)
-        rt_of[i] = kDown ? wrow0 / 16 + i : (i < 4 ? 0 : g.Fg / 16) + wrow0 / 16 + (i & 3);
+    const int n_items = a.tmeta[kDown ? 1 : 0];
+    // XCD-aware order: XCD x = pid % 8 takes the real items [x per, (x + 1) per)
+    const int per = (n_items + 7) / 8;
+    const int j = blockIdx.x / 8;
+    if (j >= per) return;
+    const int item = (blockIdx.x % 8) * per + j;
+    if (item >= n_items) return;
+    const TileItem it = reinterpret_cast<const TileItem*>(a.tmeta + 8)[(kDown ? a.tcap1 : 0) + item];
 
-    // global -> LDS copy assignment, 4 chunks of 16 B per thread per operand
-    const uint16_t* gW[4];
-    const uint16_t* gX[4];
-    int wb[4], wl[4], cr[4], cc[4];
-#pragma unroll
-    for (int i = 0; i < 4; ++i) {
-        const int c = tid + 256 * i;
-        wb[i] = c >> 6;
-        wl[i] = c & 63;
-        const int rtl = wb[i] >> 1, ks = wb[i] & 1;
-        gW[i] = (16 * rt_of[rtl] < rows_total) ? wbase + ((size_t)rt_of[rtl] * nst + ks) * 512 + wl[i] * 8 : nullptr;
-        cr[i] = c >> 3;
-        cc[i] = (c & 7) * 8;
-        const int n = n0 + cr[i];
-        gX[i] = nullptr;
-        if (!kDown) {
-            const int t = group_token(a, g, n);
-            if (t >= 0) gX[i] = static_cast<const uint16_t*>(a.x) + (size_t)t * a.H + cc[i];
-        } else if (n < g.count) {
-            gX[i] = static_cast<const uint16_t*>(a.act) + (size_t)(g.rowbase + n) * a.Fa + cc[i];
+    const int tid = threadIdx.x, lane = lane_id();
+    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+    const int wm = wave & 1, wn = wave >> 1;
+    const int K = kDown ? it.Fg : a.H;
+    const int nk = K / 32;  // slabs
+    const size_t wsize = (size_t)(kDown ? 1 : 2) * it.Fg * a.H;  // elements of one expert's matrix
+    const uint16_t* wbase;
+    if (it.wsel >= 0) wbase = static_cast<const uint16_t*>(kDown ? a.w2 : a.w13) + (size_t)it.wsel * wsize;
+    else wbase = static_cast<const uint16_t*>(kDown ? a.ws2 : a.ws13) + (size_t)(-it.wsel - 1) * wsize;
+    // phase 1: features r0 .. r0 + 127 (gate rows in LDS blocks 0..7, up rows in 8..15);
+    // phase 2: rows r0 .. r0 + 255 of W2
+    const int r0 = it.wt * (kDown ? kGM : kGM / 2);
+    const int rows_out = kDown ? a.H : it.Fg;  // rows (phase 2) or features (phase 1) that exist
+    const int n0 = it.n0;
+
+    // 16-row tile of the weight matrix held in LDS weight block b; a block past the
+    // matrix reads tile 0 instead (its rows are never stored)
+    auto row_tile = [&](int b) -> int {
+        if (kDown) {
+            const int rt = r0 / 16 + b;
+            return 16 * rt < a.H ? rt : 0;
         }
-    }
-
-    const int wr = wave >> 1, wc = wave & 1;
-    const int r = lane & 15, kq = (lane >> 4) * 8;
-    int rtl_of[4];
+        const int f16 = r0 / 16 + (b & 7);
+        if (16 * f16 >= it.Fg) return 0;
+        return b < 8 ? f16 : it.Fg / 16 + f16;
+    };
+    // this wave's loads: weight blocks 2w, 2w + 1 and token blocks 2w, 2w + 1; a token
+    // block past the group reads the group's first block instead (never stored)
+    const uint16_t* gW0 = wbase + (size_t)row_tile(2 * wave) * nk * 512 + lane * 8;
+    const uint16_t* gW1 = wbase + (size_t)row_tile(2 * wave + 1) * nk * 512 + lane * 8;
+    const uint16_t* gX[2];
 #pragma unroll
-    for (int m = 0; m < 4; ++m) rtl_of[m] = kDown ? 4 * wr + m : (m < 2 ? 2 * wr + m : 4 + 2 * wr + (m - 2));
-    f32x4 acc[4][4];
+    for (int i = 0; i < 2; ++i) {
+        const int nb = n0 / 16 + 2 * wave + i;
+        const int blk = (16 * nb < it.count) ? nb : 0;
+        if (!kDown)
+            gX[i] = static_cast<const uint16_t*>(a.xg) + (size_t)(it.xblk + blk) * (a.H / 32) * 512 + lane * 8;
+        else
+            gX[i] = static_cast<const uint16_t*>(a.act) + (size_t)(it.ablk + blk) * (a.Fa / 32) * 512 + lane * 8;
+    }
+    const uint32_t lds0 = (uint32_t)(uintptr_t)(lds_u8*)sbuf;
+    auto issue = [&](int kt, int stage) {
+        const uint32_t base = lds0 + stage * kGStageBytes;
+        lds_load_1k(base + (2 * wave) * 1024, gW0 + (size_t)kt * 512);
+        lds_load_1k(base + (2 * wave + 1) * 1024, gW1 + (size_t)kt * 512);
+        lds_load_1k(base + (16 + 2 * wave) * 1024, gX[0] + (size_t)kt * 512);
+        lds_load_1k(base + (17 + 2 * wave) * 1024, gX[1] + (size_t)kt * 512);
+    };
+
+    // operand blocks of this wave: A tile m (32 rows) = LDS weight blocks ab[m], ab[m] + 1;
+    // phase 1: m = 0, 1 gate rows, m = 2, 3 the up rows of the same features
+    int ab[4];
+#pragma unroll
+    for (int m = 0; m < 4; ++m) ab[m] = kDown ? 8 * wm + 2 * m : (m < 2 ? 4 * wm + 2 * m : 8 + 4 * wm + 2 * (m - 2));
+    // B tile jn (32 tokens) = token blocks 16 + 4 wn + 2 jn (+1).  Lane's 16-byte piece of a
+    // 32-row (or 32-token) operand at K step s of the slab: block + (l % 32) / 16, piece
+    // (l % 16) + 16 (2 s + l / 32)
+    const int half = (lane >> 4) & 1;
+    const int piece0 = (lane & 15) + 16 * (lane >> 5);
+    // a wave whose rows or tokens all lie past the group skips its MFMAs
+    const bool live = (n0 + 64 * wn < it.count) && (r0 + (kDown ? 128 : 64) * wm < rows_out);
+
+    f32x16 acc[4][2];
 #pragma unroll
     for (int m = 0; m < 4; ++m)
 #pragma unroll
-        for (int j = 0; j < 4; ++j) acc[m][j] = f32x4{0.f, 0.f, 0.f, 0.f};
+        for (int jn = 0; jn < 2; ++jn) acc[m][jn] = f32x16{};
 
-    // one LDS buffer (so three workgroups fit on a CU); slab kt + 1 is loaded
-    // into registers while slab kt is multiplied out of LDS
-    const int nk = K / kTk;
-    u32x4 rw[4], rx[4];
-    auto gload = [&](int kt) {
 #pragma unroll
-        for (int i = 0; i < 4; ++i) {
-            rw[i] = gW[i] ? *reinterpret_cast<const u32x4*>(gW[i] + (size_t)kt * 2 * 512) : u32x4{0u, 0u, 0u, 0u};
-            rx[i] = gX[i] ? *reinterpret_cast<const u32x4*>(gX[i] + kt * kTk) : u32x4{0u, 0u, 0u, 0u};
-        }
-    };
-    gload(0);
+    for (int st = 0; st < kGStages - 1; ++st)
+        if (st < nk) issue(st, st);
+
+    int stage = 0;
     for (int kt = 0; kt < nk; ++kt) {
+        // slabs issued after kt: min(kGStages - 2, nk - 1 - kt), four loads each
+        const int later = nk - 1 - kt;
+        if (later >= 3) wait_then_barrier<12>();
+        else if (later == 2) wait_then_barrier<8>();
+        else if (later == 1) wait_then_barrier<4>();
+        else wait_then_barrier<0>();
+        // every wave is past slab kt - 1: its stage may be refilled
+        if (kt + kGStages - 1 < nk) issue(kt + kGStages - 1, stage == 0 ? kGStages - 1 : stage - 1);
+        if (live) {
+            const uint8_t* sp = sbuf + stage * kGStageBytes;
 #pragma unroll
-        for (int i = 0; i < 4; ++i) {
-            *reinterpret_cast<u32x4*>(&sW[wb[i]][wl[i] * 8]) = rw[i];
-            *reinterpret_cast<u32x4*>(&sX[cr[i]][cc[i]]) = rx[i];
+            for (int ks = 0; ks < 2; ++ks) {
+                const int off = 16 * (piece0 + 32 * ks) + 1024 * half;
+                bf16x8 A[4], B[2];
+#pragma unroll
+                for (int m = 0; m < 4; ++m)
+                    A[m] = __builtin_bit_cast(bf16x8, *reinterpret_cast<const u32x4*>(sp + ab[m] * 1024 + off));
+#pragma unroll
+                for (int jn = 0; jn < 2; ++jn)
+                    B[jn] = __builtin_bit_cast(
+                        bf16x8, *reinterpret_cast<const u32x4*>(sp + (16 + 4 * wn + 2 * jn) * 1024 + off));
+#pragma unroll
+                for (int m = 0; m < 4; ++m)
+#pragma unroll
+                    for (int jn = 0; jn < 2; ++jn) acc[m][jn] = mfma32x32x16(A[m], B[jn], acc[m][jn]);
+            }
         }
-        __syncthreads();
-        if (kt + 1 < nk) gload(kt + 1);
-#pragma unroll
-        for (int ks = 0; ks < kTk / 32; ++ks) {
-            bf16x8 A[4], B[4];
-#pragma unroll
-            for (int m = 0; m < 4; ++m)
-                A[m] = __builtin_bit_cast(bf16x8, *reinterpret_cast<const u32x4*>(&sW[rtl_of[m] * 2 + ks][lane * 8]));
-#pragma unroll
-            for (int j = 0; j < 4; ++j)
-                B[j] = __builtin_bit_cast(bf16x8, *reinterpret_cast<const u32x4*>(&sX[64 * wc + 16 * j + r][ks * 32 + kq]));
-#pragma unroll
-            for (int m = 0; m < 4; ++m)
-#pragma unroll
-                for (int j = 0; j < 4; ++j) acc[m][j] = mfma16x16x32(A[m], B[j], acc[m][j]);
-        }
-        __syncthreads();
+        stage = stage == kGStages - 1 ? 0 : stage + 1;
     }
-
+    // Epilogue through the (now idle) LDS ring, so that the global stores are whole
+    // rows or whole tile-layout blocks instead of 8-byte pieces of 32 token rows.
+    // Lane holds column (token) l % 32 of each 32 x 32 tile, rows 8 (v / 4) + 4 (l / 32) + v % 4.
+    __syncthreads();  // every wave is done with the last stage
+    if (!kDown) {
+        // phase 1: act = silu(gate) * up in bf16, staged in the tile layout of its 16 x 4
+        // blocks (token block tb, feature block fb at LDS block 4 tb + fb)
 #pragma unroll
-    for (int j = 0; j < 4; ++j) {
-        const int n = n0 + 64 * wc + 16 * j + r;
-        if (n >= g.count) continue;
-        if (!kDown) {
-            // acc[m] = gate, acc[m + 2] = up, features wrow0 + 16 (2 wr + m) + 4 (lane/16) + i
+        for (int jn = 0; jn < 2; ++jn) {
+            const int nl = 64 * wn + 32 * jn + (lane & 31);  // token within the item
 #pragma unroll
-            for (int m = 0; m < 2; ++m) {
-                const f32x4 gv = acc[m][j], uv = acc[m + 2][j];
-                const int f = wrow0 + 16 * (2 * wr + m) + 4 * (lane >> 4);
-                if (f >= g.Fg) continue;
-                u32x2 packed;
-                packed.x = pack_bf16x2(silu(gv.x) * uv.x, silu(gv.y) * uv.y);
-                packed.y = pack_bf16x2(silu(gv.z) * uv.z, silu(gv.w) * uv.w);
-                *reinterpret_cast<u32x2*>(static_cast<uint16_t*>(a.act) + (size_t)(g.rowbase + n) * a.Fa + f) = packed;
-            }
-        } else {
+            for (int m = 0; m < 2; ++m)
 #pragma unroll
-            for (int m = 0; m < 4; ++m) {
-                const int h = wrow0 + 16 * (4 * wr + m) + 4 * (lane >> 4);
-                if (h < a.H) *reinterpret_cast<f32x4*>(a.y + (size_t)(g.rowbase + n) * a.H + h) = acc[m][j];
-            }
+                for (int q = 0; q < 4; ++q) {
+                    const int fl = 64 * wm + 32 * m + 8 * q + 4 * (lane >> 5);  // feature within the item
+                    const f32x16 gv = acc[m][jn], uv = acc[m + 2][jn];
+                    u32x2 packed;
+                    packed.x = pack_bf16x2(silu(gv[4 * q]) * uv[4 * q], silu(gv[4 * q + 1]) * uv[4 * q + 1]);
+                    packed.y = pack_bf16x2(silu(gv[4 * q + 2]) * uv[4 * q + 2], silu(gv[4 * q + 3]) * uv[4 * q + 3]);
+                    const int off = ((nl >> 4) * 4 + (fl >> 5)) * 1024 + 16 * ((nl & 15) + 16 * ((fl & 31) >> 3)) +
+                                    2 * (fl & 7);
+                    *reinterpret_cast<u32x2*>(sbuf + off) = packed;
+                }
+        }
+        __syncthreads();
+        // 64 blocks of 1 KB; a block goes out if it holds rows of the group and features that exist
+        uint16_t* act = static_cast<uint16_t*>(a.act);
+        for (int c = tid; c < 64 * 64; c += 512) {
+            const int blk = c >> 6, piece = c & 63;
+            const int tb = blk >> 2, fb = blk & 3;
+            if (n0 + 16 * tb >= it.count || r0 + 32 * fb >= it.Fg) continue;
+            const u32x4 v = *reinterpret_cast<const u32x4*>(sbuf + blk * 1024 + 16 * piece);
+            *reinterpret_cast<u32x4*>(act + ((size_t)(it.ablk + n0 / 16 + tb) * (a.Fa / 32) + r0 / 32 + fb) * 512 +
+                                      8 * piece) = v;
+        }
+    } else {
+        // phase 2: expert outputs in bf16, rounded once (the combine sums them in fp32),
+        // staged as 256 token rows of 256 outputs (pitch 264 elements)
+        constexpr int kPitch = 264;
+        uint16_t* sy = reinterpret_cast<uint16_t*>(sbuf);
+#pragma unroll
+        for (int jn = 0; jn < 2; ++jn) {
+            const int nl = 64 * wn + 32 * jn + (lane & 31);
+#pragma unroll
+            for (int m = 0; m < 4; ++m)
+#pragma unroll
+                for (int q = 0; q < 4; ++q) {
+                    const int hl = 128 * wm + 32 * m + 8 * q + 4 * (lane >> 5);
+                    const f32x16 v = acc[m][jn];
+                    u32x2 packed;
+                    packed.x = pack_bf16x2(v[4 * q], v[4 * q + 1]);
+                    packed.y = pack_bf16x2(v[4 * q + 2], v[4 * q + 3]);
+                    *reinterpret_cast<u32x2*>(sy + nl * kPitch + hl) = packed;
+                }
+        }
+        __syncthreads();
+        // 256 rows x 32 pieces of 16 bytes; rows of the group, outputs that exist
+        for (int c = tid; c < 256 * 32; c += 512) {
+            const int nl = c >> 5, piece = c & 31;
+            const int h = r0 + 8 * piece;
+            if (n0 + nl >= it.count || h >= a.H) continue;
+            const u32x4 v = *reinterpret_cast<const u32x4*>(sy + nl * kPitch + 8 * piece);
+            *reinterpret_cast<u32x4*>(a.y16 + (size_t)(it.rowbase + n0 + nl) * a.H + h) = v;
         }
     }
 }
@@ -656,11 +868,13 @@ __global__ void __launch_bounds__(256) k_ffn2_f32(Args a) {
     }
 }
 
-// y_out[p] = sum_c y[c][p] for resident packed rows p < n_res and all shared rows.
+// y_out[p] = sum_c y[c][p] for resident packed rows p < n_res and all shared rows
+// (kInBf16: a single chunk of bf16 rows, widened).
+template <bool kInBf16>
 __global__ void __launch_bounds__(256) k_reduce_splits(int T, int H, int E, int k, int S, int slots,
                                                        const int32_t* __restrict__ counts,
                                                        const int32_t* __restrict__ expert_slot,
-                                                       const float* __restrict__ y, int ks, long long stride,
+                                                       const void* __restrict__ y_in, int ks, long long stride,
                                                        float* __restrict__ y_out) {
     __shared__ int s_nres;
     if (threadIdx.x == 0) {
@@ -673,6 +887,14 @@ __global__ void __launch_bounds__(256) k_reduce_splits(int T, int H, int E, int 
     const int P = T * k, rows = P + S * T;
     const int row = blockIdx.x;
     if (row >= rows || (row < P && row >= s_nres)) return;
+    if constexpr (kInBf16) {
+        const uint16_t* y = static_cast<const uint16_t*>(y_in);
+        for (int h = threadIdx.x * 4; h < H; h += 1024)
+            *reinterpret_cast<f32x4*>(y_out + (size_t)row * H + h) =
+                bf16x4_to_f32(*reinterpret_cast<const u32x2*>(y + (size_t)row * H + h));
+        return;
+    }
+    const float* y = static_cast<const float*>(y_in);
     for (int h = threadIdx.x * 4; h < H; h += 1024) {
         constexpr int kMax = 16;  // same order as the combine: chunk 0, then 1, ...
         f32x4 p[kMax];
@@ -724,6 +946,72 @@ bool stream_weights(const Shape& s) {
 
 bool ffn_packs_offloaded(const Shape& s) { return use_stream(s) || s.bf16; }
 
+namespace {
+// bf16 prefill: row blocks of the routed groups padded to 16 rows (at most 15 pad
+// rows per group) and of the batch in order
+long long tiled_routed_rows(const Shape& s) {
+    return (long long)s.T * s.k + 15ll * max_routed_groups(s);
+}
+long long tiled_t16(const Shape& s) { return (s.T + 15) / 16 * 16ll; }
+bool use_tiled(const Shape& s) { return s.bf16 && !use_stream(s); }
+
+// Worst-case items of a tiled phase: the routed groups have at most ceil(P / 256)
+// full 256-row tiles plus one partial tile each
+long long tiled_items(const Shape& s, bool down) {
+    const long long P = (long long)s.T * s.k;
+    const long long G = max_routed_groups(s);
+    const long long rt = G == 0 ? 0 : (P + kGN - 1) / kGN + G;
+    const long long tps = (s.T + kGN - 1) / kGN;
+    if (down) return (rt + (long long)s.S * tps) * ((s.H + kGM - 1) / kGM);
+    const long long wt_r = (s.F + kGM / 2 - 1) / (kGM / 2), wt_s = s.S > 0 ? (s.Fs + kGM / 2 - 1) / (kGM / 2) : 0;
+    return rt * wt_r + (long long)s.S * tps * wt_s;
+}
+
+Args make_args(const Shape& s, const FfnArgs& fa) {
+    Args a;
+    a.T = s.T; a.H = s.H; a.E = s.E; a.F = s.F; a.k = s.k; a.S = s.S; a.Fs = s.Fs; a.slots = s.slots;
+    a.x = fa.x; a.perm = fa.perm; a.counts = fa.counts; a.seg_start = fa.seg_start; a.expert_slot = fa.expert_slot;
+    a.w13 = fa.w13; a.w2 = fa.w2; a.ws13 = fa.ws13; a.ws2 = fa.ws2;
+    a.act = fa.act; a.Fa = fa.Fa; a.y = fa.y; a.ks = fa.ks; a.y_ks_stride = fa.y_ks_stride;
+    a.max_routed = max_routed_groups(s);
+    a.ipg_r = a.ipg_s = 0;
+    a.topk_w = fa.topk_w;
+    a.n_res = fa.n_res;
+    a.off_rows = fa.off_rows;
+    a.off_w = fa.off_w;
+    a.xg = fa.xg;
+    a.tmeta = fa.tmeta;
+    a.tcap1 = use_tiled(s) ? (int)tiled_items(s, false) : 0;
+    a.y16 = static_cast<uint16_t*>(fa.y16);
+    return a;
+}
+}  // namespace
+
+long long ffn_act_rows(const Shape& s) {
+    if (use_tiled(s)) return tiled_routed_rows(s) + (long long)s.S * tiled_t16(s);
+    return (long long)s.T * s.k + (long long)s.S * s.T;
+}
+
+long long ffn_gather_rows(const Shape& s) {
+    if (!use_tiled(s)) return 0;
+    return tiled_routed_rows(s) + (s.S > 0 ? tiled_t16(s) : 0);
+}
+
+size_t ffn_tile_meta_bytes(const Shape& s) {
+    if (!use_tiled(s)) return 0;
+    return 32 + sizeof(TileItem) * (size_t)(tiled_items(s, false) + tiled_items(s, true));
+}
+
+hipError_t launch_gather_tokens(const Shape& s, const FfnArgs& fa, hipStream_t st) {
+    if (s.T == 0 || !use_tiled(s)) return hipSuccess;
+    const Args a = make_args(s, fa);
+    const long long blocks = ffn_gather_rows(s) / 16;
+    const int P = s.T * s.k;
+    const int n_pack = (fa.off_rows || fa.off_w) ? (P < 256 ? P : 256) : 0;
+    hipLaunchKernelGGL(k_gather_tokens, dim3((unsigned)(blocks + n_pack)), dim3(256), 0, st, a, (int)blocks);
+    return hipGetLastError();
+}
+
 int ffn_down_splits(const Shape& s) {
     if (!use_stream(s)) return 1;
     // Phase-2 work items: (groups) x (H / rows) x ks, each streaming `rows` rows
@@ -755,16 +1043,7 @@ hipError_t launch_grouped_ffn(const Shape& s, const FfnArgs& fa, hipStream_t st,
         if (e == hipSuccess && between) e = hipEventRecord(between, st);
         return e;
     };
-    Args a;
-    a.T = s.T; a.H = s.H; a.E = s.E; a.F = s.F; a.k = s.k; a.S = s.S; a.Fs = s.Fs; a.slots = s.slots;
-    a.x = fa.x; a.perm = fa.perm; a.counts = fa.counts; a.seg_start = fa.seg_start; a.expert_slot = fa.expert_slot;
-    a.w13 = fa.w13; a.w2 = fa.w2; a.ws13 = fa.ws13; a.ws2 = fa.ws2;
-    a.act = fa.act; a.Fa = fa.Fa; a.y = fa.y; a.ks = fa.ks; a.y_ks_stride = fa.y_ks_stride;
-    a.max_routed = max_routed_groups(s);
-    a.topk_w = fa.topk_w;
-    a.n_res = fa.n_res;
-    a.off_rows = fa.off_rows;
-    a.off_w = fa.off_w;
+    Args a = make_args(s, fa);
     if (!s.bf16 && !use_stream(s)) {  // fp32 prefill: plain FMA kernels
         a.ipg_r = a.ipg_s = 1;
         const int groups = a.max_routed + s.S;
@@ -802,39 +1081,41 @@ hipError_t launch_grouped_ffn(const Shape& s, const FfnArgs& fa, hipStream_t st,
         }
         return hipGetLastError();
     }
-    // tiled: worst-case number of kTn-token tiles over the routed groups
-    const int P = s.T * s.k;
-    const int max_rtiles = (a.max_routed == 0) ? 0 : (P + kTn - 1) / kTn + a.max_routed;
-    const int tps = (s.T + kTn - 1) / kTn;
-    a.ipg_r = a.ipg_s = 0;
+    // tiled: a workgroup per worst-case item (the table the token gather wrote holds the
+    // real ones, which the kernel maps over the XCDs); the offloaded rows were packed
+    // by the token gather
     auto round8 = [](long long n) { return (n + 7) / 8 * 8; };
     {
-        const int ntn_r = s.F / 64, ntn_s = s.S > 0 ? s.Fs / 64 : 1;
-        const long long grid = round8((long long)max_rtiles * ntn_r + (long long)s.S * tps * ntn_s);
-        // pack workgroups after the items: dispatched last, they overlap the phase's tail
-        const int n_pack = (fa.off_rows || fa.off_w) ? (P < 256 ? P : 256) : 0;
-        if (grid + n_pack > 0)
-            hipLaunchKernelGGL((k_ffn_tiled<false>), dim3((unsigned)(grid + n_pack)), dim3(256), 0, st, a, max_rtiles,
-                               ntn_r, ntn_s, (int)grid);
+        const long long grid = round8(tiled_items(s, false));
+        if (grid > 0) hipLaunchKernelGGL((k_ffn_tiled<false>), dim3((unsigned)grid), dim3(512), 0, st, a);
     }
     if (hipError_t e = mark(); e != hipSuccess) return e;
     {
-        const int ntn = (s.H + 127) / 128;
-        const long long grid = round8((long long)max_rtiles * ntn + (long long)s.S * tps * ntn);
-        if (grid > 0)
-            hipLaunchKernelGGL((k_ffn_tiled<true>), dim3((unsigned)grid), dim3(256), 0, st, a, max_rtiles, ntn, ntn,
-                               (int)grid);
+        const long long grid = round8(tiled_items(s, true));
+        if (grid > 0) hipLaunchKernelGGL((k_ffn_tiled<true>), dim3((unsigned)grid), dim3(512), 0, st, a);
     }
     return hipGetLastError();
 }
 
-hipError_t launch_reduce_splits(const Shape& s, const int32_t* counts, const int32_t* expert_slot, const float* y,
-                                int ks, long long y_ks_stride, float* y_out, hipStream_t st) {
+hipError_t launch_reduce_splits(const Shape& s, const int32_t* counts, const int32_t* expert_slot, const void* y,
+                                bool y_bf16, int ks, long long y_ks_stride, float* y_out, hipStream_t st) {
     const int rows = s.T * s.k + s.S * s.T;
     if (rows == 0) return hipSuccess;
-    hipLaunchKernelGGL(k_reduce_splits, dim3(rows), dim3(256), 0, st, s.T, s.H, s.E, s.k, s.S, s.slots, counts,
-                       expert_slot, y, ks, y_ks_stride, y_out);
+    if (y_bf16)
+        hipLaunchKernelGGL(k_reduce_splits<true>, dim3(rows), dim3(256), 0, st, s.T, s.H, s.E, s.k, s.S, s.slots,
+                           counts, expert_slot, y, 1, y_ks_stride, y_out);
+    else
+        hipLaunchKernelGGL(k_reduce_splits<false>, dim3(rows), dim3(256), 0, st, s.T, s.H, s.E, s.k, s.S, s.slots,
+                           counts, expert_slot, y, ks, y_ks_stride, y_out);
     return hipGetLastError();
+}
+
+bool ffn_y_bf16(const Shape& s) { return use_tiled(s); }
+
+size_t ffn_y_bytes(const Shape& s) {
+    const long long rows = (long long)s.T * s.k + (long long)s.S * s.T;
+    if (ffn_y_bf16(s)) return (size_t)rows * s.H * 2;
+    return (size_t)ffn_down_splits(s) * rows * s.H * 4;
 }
 
 }  // namespace saem

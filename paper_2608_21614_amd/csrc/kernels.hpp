@@ -47,14 +47,38 @@ struct FfnArgs {
     float* y;           // [ks][rows][H] fp32 partial sums over K chunks of the down projection
     int ks;             // number of K chunks of the down projection
     long long y_ks_stride;
-    // optional: pack the offloaded rows in extra workgroups of phase 1 (decode path only)
+    // optional: pack the offloaded rows in extra workgroups (of phase 1 at decode,
+    // of the token gather at bf16 prefill)
     const float* topk_w = nullptr;
     const int32_t* n_res = nullptr;
     void* off_rows = nullptr;
     float* off_w = nullptr;
+    // bf16 prefill: the token rows gathered into the MFMA tile layout, ffn_gather_rows(s) x H,
+    // and the tiled kernels' item tables (ffn_tile_meta_bytes(s), 32-byte aligned)
+    void* xg = nullptr;
+    int32_t* tmeta = nullptr;
+    // bf16 prefill: phase 2 writes the expert outputs here in bf16 ([rows][H]) instead of y
+    void* y16 = nullptr;
 };
 
-// True when the FFN can fold the offloaded-row pack into its phase-1 launch.
+// True when the expert outputs are bf16 (y16) rather than fp32 partial sums (y).
+bool ffn_y_bf16(const Shape& s);
+// Bytes of the expert-output buffer: bf16 rows, or ks fp32 chunks of rows.
+size_t ffn_y_bytes(const Shape& s);
+
+// Rows of the activation buffer (row stride Fa; the bf16 prefill path pads every
+// group to 16 rows) and of the gathered-token buffer (0: the path has none).
+long long ffn_act_rows(const Shape& s);
+long long ffn_gather_rows(const Shape& s);
+size_t ffn_tile_meta_bytes(const Shape& s);
+
+// bf16 prefill: gathers the resident groups' token rows (and the batch in order,
+// for the shared experts) into a.xg, and packs the offloaded rows if asked;
+// must precede launch_grouped_ffn on the stream.  No-op on the other paths.
+hipError_t launch_gather_tokens(const Shape& s, const FfnArgs& a, hipStream_t st);
+
+// True when the FFN path packs the offloaded rows itself (in phase 1 at decode,
+// in the token gather at bf16 prefill).
 bool ffn_packs_offloaded(const Shape& s);
 
 // Number of K chunks the down projection is split into (1 = direct sums).
@@ -62,13 +86,14 @@ int ffn_down_splits(const Shape& s);
 // Launches phase 1 then phase 2; records `between` (if not null) after phase 1.
 hipError_t launch_grouped_ffn(const Shape& s, const FfnArgs& a, hipStream_t st, hipEvent_t between = nullptr);
 
-// y_out[p] = sum_c y[c][p] for the resident packed rows and the shared rows.
-hipError_t launch_reduce_splits(const Shape& s, const int32_t* counts, const int32_t* expert_slot, const float* y,
-                                int ks, long long y_ks_stride, float* y_out, hipStream_t st);
+// y_out[p] = sum_c y[c][p] for the resident packed rows and the shared rows (y_bf16:
+// one chunk of bf16 rows, widened to fp32).
+hipError_t launch_reduce_splits(const Shape& s, const int32_t* counts, const int32_t* expert_slot, const void* y,
+                                bool y_bf16, int ks, long long y_ks_stride, float* y_out, hipStream_t st);
 
-// Deterministic combine back to token order.
+// Deterministic combine back to token order.  y: ks fp32 chunks, or (y_bf16) one chunk of bf16 rows.
 hipError_t launch_combine(const Shape& s, const int32_t* topk_idx, const float* topk_w, const int32_t* inv_perm,
-                          const int32_t* expert_slot, const float* y, int ks, long long y_ks_stride,
+                          const int32_t* expert_slot, const void* y, bool y_bf16, int ks, long long y_ks_stride,
                           const float* y_off, const int32_t* n_res, void* out, bool out_bf16, hipStream_t st);
 
 // Row-major [rows, K] -> tile layout.
