@@ -219,7 +219,8 @@ moe_status moe_combine(const moe_dims* dims, const int32_t* topk_idx, const floa
         return MOE_ERR_INVALID_ARG;
     if (y_off && !ok_ptr4(n_res)) return MOE_ERR_INVALID_ARG;
     const Shape s = shape_of(dims);
-    return hip_status(saem::launch_combine(s, topk_idx, topk_w, inv_perm, expert_slot, y, false, 1, 0, y_off, n_res,
+    return hip_status(saem::launch_combine(s, topk_idx, topk_w, inv_perm, expert_slot, y, false, 1, 0, y_off,
+                                           y_off ? n_res : nullptr,
                                            out, out_dtype == MOE_BF16, static_cast<hipStream_t>(stream)));
 }
 
@@ -301,7 +302,7 @@ static moe_status layer_forward(const moe_layer_args* a, void* ws, size_t ws_byt
     if (e == hipSuccess) e = mark(saem::launch_grouped_ffn(s, f, hs, ev[4]), 5);
     if (e == hipSuccess)
         e = mark(saem::launch_combine(s, idx, w, inv, a->expert_slot, at<char>(ws, L.y), y16, L.ks, f.y_ks_stride,
-                                      nullptr, nullptr,
+                                      nullptr, nres,
                                       a->out, a->out_dtype == MOE_BF16, hs), 6);
     return hip_status(e);
 }

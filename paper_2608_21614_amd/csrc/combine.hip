@@ -55,7 +55,10 @@ __global__ void __launch_bounds__(256)
     const int h = (blockIdx.y * 256 + threadIdx.x) * 4;
     if (h >= H) return;
     const int P = T * k;
-    const int nres = y_off ? *n_res_p : 0;
+    // with n_res at hand, a choice is resident iff its packed row lies in the resident
+    // prefix [0, n_res) (the repacking puts resident pairs first), which spares a round
+    // trip to expert_slot
+    const int nres = n_res_p ? *n_res_p : 0;
 
     // the token's choices
     int e[kK], p[kK];
@@ -77,7 +80,8 @@ __global__ void __launch_bounds__(256)
     for (int j = 0; j < kK; ++j) {
         src[j] = 0;
         if (j < k && e[j] >= 0 && e[j] < E && p[j] >= 0 && p[j] < P) {
-            if (is_resident(expert_slot[e[j]], slots)) src[j] = 1;
+            const bool res = n_res_p ? p[j] < nres : is_resident(expert_slot[e[j]], slots);
+            if (res) src[j] = 1;
             else if (y_off && p[j] >= nres) src[j] = 2;
         }
     }

@@ -610,16 +610,27 @@ __global__ void __launch_bounds__(256) k_gather_tokens(Args a, int blocks_max) {
     }
     __syncthreads();
     if (pid >= rb_routed && (a.S == 0 || pid - rb_routed >= (a.T + 15) / 16)) return;
-    // 16-byte piece j of block c: row j % 16, columns 32 c + 8 (j / 16) .. + 7
+    // 16-byte piece j of block c: row j % 16, columns 32 c + 8 (j / 16) .. + 7; a batch's
+    // loads all go out before its stores (one memory round trip per batch, not per piece)
     const int nc = a.H / 32;
     const uint16_t* x = static_cast<const uint16_t*>(a.x);
     u32x4* dst = reinterpret_cast<u32x4*>(static_cast<uint16_t*>(a.xg) + (size_t)pid * nc * 512);
-    for (int idx = threadIdx.x; idx < nc * 64; idx += 256) {
-        const int c = idx >> 6, j = idx & 63;
-        const int t = s_tok[j & 15];
-        u32x4 v = {0u, 0u, 0u, 0u};
-        if (t >= 0) v = *reinterpret_cast<const u32x4*>(x + (size_t)t * a.H + 32 * c + 8 * (j >> 4));
-        dst[idx] = v;
+    constexpr int kBatch = 16;
+    for (int base = 0; base < nc * 64; base += 256 * kBatch) {
+        u32x4 v[kBatch];
+#pragma unroll
+        for (int u = 0; u < kBatch; ++u) {
+            const int idx = base + 256 * u + threadIdx.x;
+            const int c = idx >> 6, j = idx & 63;
+            const int t = idx < nc * 64 ? s_tok[j & 15] : -1;
+            v[u] = u32x4{0u, 0u, 0u, 0u};
+            if (t >= 0) v[u] = *reinterpret_cast<const u32x4*>(x + (size_t)t * a.H + 32 * c + 8 * (j >> 4));
+        }
+#pragma unroll
+        for (int u = 0; u < kBatch; ++u) {
+            const int idx = base + 256 * u + threadIdx.x;
+            if (idx < nc * 64) dst[idx] = v[u];
+        }
     }
 }
 
