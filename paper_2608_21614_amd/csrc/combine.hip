@@ -3,7 +3,8 @@
 // runs give bitwise-identical outputs; the paper's atomic accumulation is not
 // reproducible (Section V-C).
 //
-// Workgroup = one token x 1024 hidden columns (4 per thread, 16-byte loads):
+// Workgroup = one token x 1024 hidden columns (4 per thread, 16-byte loads of fp32
+// expert outputs; 2048 columns, 8 per thread, when they come in bf16):
 //   acc = 0  (fp32)
 //   for j in 0..k-1:  acc += w[t,j] * (sum_c y[c][inv[t,j]])          resident
 //                     acc += w[t,j] * y_off[inv[t,j] - n_res]          offloaded, if given
@@ -36,20 +37,12 @@ __device__ __forceinline__ f32x4 sum_chunks(const float* __restrict__ y, int ks,
 // then the sums run in the fixed order above.  KS >= ks is the compile-time
 // bound on the K chunks; above two chunks the loads go one contribution at a
 // time (all of its chunks together), which keeps the registers in bounds.
-template <bool kOutBf16, int KS, bool kYBf16 = false>
+template <bool kOutBf16, int KS>
 __global__ void __launch_bounds__(256)
     k_combine(int T, int H, int E, int k, int S, int slots, const int32_t* __restrict__ topk_idx,
               const float* __restrict__ topk_w, const int32_t* __restrict__ inv_perm,
-              const int32_t* __restrict__ expert_slot, const void* __restrict__ y_any, int ks, long long stride,
+              const int32_t* __restrict__ expert_slot, const float* __restrict__ y, int ks, long long stride,
               const float* __restrict__ y_off, const int32_t* __restrict__ n_res_p, void* __restrict__ out) {
-    static_assert(!kYBf16 || KS == 1, "bf16 expert outputs come in one chunk");
-    const float* __restrict__ y = static_cast<const float*>(y_any);
-    const uint16_t* __restrict__ y16 = static_cast<const uint16_t*>(y_any);
-    // four consecutive outputs of row r at column h of the expert outputs
-    auto yrow4 = [&](size_t off) -> f32x4 {
-        if constexpr (kYBf16) return bf16x4_to_f32(*reinterpret_cast<const u32x2*>(y16 + off));
-        else return *reinterpret_cast<const f32x4*>(y + off);
-    };
     constexpr int kK = 8, kS = 8;  // bounds on k and S (the ABI checks both)
     const int t = blockIdx.x;
     const int h = (blockIdx.y * 256 + threadIdx.x) * 4;
@@ -93,19 +86,12 @@ __global__ void __launch_bounds__(256)
 #pragma unroll
         for (int j = 0; j < kK; ++j) {
             const size_t off = (size_t)(src[j] ? p[j] : 0) * H + h;
-            if constexpr (kYBf16) {
-                // one chunk; a row from y_off (fp32) or from the bf16 expert outputs
-                const f32x4 l = (src[j] == 2) ? *reinterpret_cast<const f32x4*>(y_off + (off - (size_t)nres * H))
-                                              : yrow4(off);
-                v[j][0] = src[j] ? l : zero;
-            } else {
-                const float* base = (src[j] == 2) ? y_off + (off - (size_t)nres * H) : y + off;
+            const float* base = (src[j] == 2) ? y_off + (off - (size_t)nres * H) : y + off;
 #pragma unroll
-                for (int c = 0; c < KS; ++c) {
-                    const bool use = src[j] == 1 ? c < ks : (src[j] == 2 && c == 0);
-                    const f32x4 l = *reinterpret_cast<const f32x4*>(base + (use ? c * stride : 0));
-                    v[j][c] = use ? l : zero;
-                }
+            for (int c = 0; c < KS; ++c) {
+                const bool use = src[j] == 1 ? c < ks : (src[j] == 2 && c == 0);
+                const f32x4 l = *reinterpret_cast<const f32x4*>(base + (use ? c * stride : 0));
+                v[j][c] = use ? l : zero;
             }
         }
 #pragma unroll
@@ -114,7 +100,7 @@ __global__ void __launch_bounds__(256)
 #pragma unroll
             for (int c = 0; c < KS; ++c) {
                 const bool use = s2 < S && c < ks;
-                const f32x4 l = yrow4(off + (use ? c * stride : 0));
+                const f32x4 l = *reinterpret_cast<const f32x4*>(y + off + (use ? c * stride : 0));
                 vs[s2][c] = use ? l : zero;
             }
         }
@@ -150,6 +136,91 @@ __global__ void __launch_bounds__(256)
     }
 }
 
+// The same merge when the expert outputs come in bf16 (one chunk): 8 columns per
+// thread, so that every row load is 16 bytes; workgroup = one token x 2048 columns.
+template <bool kOutBf16>
+__global__ void __launch_bounds__(256)
+    k_combine_y16(int T, int H, int E, int k, int S, int slots, const int32_t* __restrict__ topk_idx,
+                  const float* __restrict__ topk_w, const int32_t* __restrict__ inv_perm,
+                  const int32_t* __restrict__ expert_slot, const uint16_t* __restrict__ y16,
+                  const float* __restrict__ y_off, const int32_t* __restrict__ n_res_p, void* __restrict__ out) {
+    constexpr int kK = 8, kS = 8;  // bounds on k and S (the ABI checks both)
+    const int t = blockIdx.x;
+    const int h = (blockIdx.y * 256 + threadIdx.x) * 8;
+    if (h >= H) return;
+    const int P = T * k;
+    const int nres = n_res_p ? *n_res_p : 0;
+    int e[kK], p[kK];
+    float w[kK];
+#pragma unroll
+    for (int j = 0; j < kK; ++j) {
+        e[j] = -1;
+        p[j] = -1;
+        w[j] = 0.f;
+        if (j < k) {
+            e[j] = topk_idx[t * k + j];
+            p[j] = inv_perm[t * k + j];
+            w[j] = topk_w[t * k + j];
+        }
+    }
+    int src[kK];  // 1 = y16 (resident), 2 = y_off (offloaded, given), 0 = nowhere
+#pragma unroll
+    for (int j = 0; j < kK; ++j) {
+        src[j] = 0;
+        if (j < k && e[j] >= 0 && e[j] < E && p[j] >= 0 && p[j] < P) {
+            const bool res = n_res_p ? p[j] < nres : is_resident(expert_slot[e[j]], slots);
+            if (res) src[j] = 1;
+            else if (y_off && p[j] >= nres) src[j] = 2;
+        }
+    }
+    // every load first (a contribution that does not apply reads row 0 and is dropped)
+    u32x4 v[kK], vs[kS];
+    f32x4 vo[kK][2];
+#pragma unroll
+    for (int j = 0; j < kK; ++j) {
+        const size_t off = (size_t)(src[j] == 1 ? p[j] : 0) * H + h;
+        v[j] = *reinterpret_cast<const u32x4*>(y16 + off);
+        if (src[j] == 2) {
+            const float* r = y_off + (size_t)(p[j] - nres) * H + h;
+            vo[j][0] = *reinterpret_cast<const f32x4*>(r);
+            vo[j][1] = *reinterpret_cast<const f32x4*>(r + 4);
+        }
+    }
+#pragma unroll
+    for (int s2 = 0; s2 < kS; ++s2)
+        vs[s2] = *reinterpret_cast<const u32x4*>(y16 + (size_t)(s2 < S ? P + s2 * T + t : 0) * H + h);
+    const f32x4 zero = {0.f, 0.f, 0.f, 0.f};
+    f32x4 lo = zero, hi = zero;
+#pragma unroll
+    for (int j = 0; j < kK; ++j) {
+        if (src[j] == 1) {
+            lo += w[j] * bf16x4_to_f32(u32x2{v[j].x, v[j].y});
+            hi += w[j] * bf16x4_to_f32(u32x2{v[j].z, v[j].w});
+        } else if (src[j] == 2) {
+            lo += w[j] * vo[j][0];
+            hi += w[j] * vo[j][1];
+        }
+    }
+#pragma unroll
+    for (int s2 = 0; s2 < kS; ++s2) {
+        if (s2 >= S) continue;
+        lo += bf16x4_to_f32(u32x2{vs[s2].x, vs[s2].y});
+        hi += bf16x4_to_f32(u32x2{vs[s2].z, vs[s2].w});
+    }
+    if (kOutBf16) {
+        u32x4 packed;
+        packed.x = pack_bf16x2(lo.x, lo.y);
+        packed.y = pack_bf16x2(lo.z, lo.w);
+        packed.z = pack_bf16x2(hi.x, hi.y);
+        packed.w = pack_bf16x2(hi.z, hi.w);
+        *reinterpret_cast<u32x4*>(static_cast<uint16_t*>(out) + (size_t)t * H + h) = packed;
+    } else {
+        float* o = static_cast<float*>(out) + (size_t)t * H + h;
+        *reinterpret_cast<f32x4*>(o) = lo;
+        *reinterpret_cast<f32x4*>(o + 4) = hi;
+    }
+}
+
 __global__ void k_stage_accumulate(int E, const int32_t* __restrict__ counts, int64_t* __restrict__ log) {
     const int e = blockIdx.x * blockDim.x + threadIdx.x;
     if (e < E) log[e] += counts[e];
@@ -159,13 +230,17 @@ template <bool kOutBf16>
 hipError_t launch_combine_ks(dim3 grid, const Shape& s, const int32_t* topk_idx, const float* topk_w,
                              const int32_t* inv_perm, const int32_t* expert_slot, const void* y, bool y_bf16, int ks,
                              long long stride, const float* y_off, const int32_t* n_res, void* out, hipStream_t st) {
-#define SAEM_COMBINE(KS, YB)                                                                                        \
-    hipLaunchKernelGGL((k_combine<kOutBf16, KS, YB>), grid, dim3(256), 0, st, s.T, s.H, s.E, s.k, s.S, s.slots,  \
-                       topk_idx, topk_w, inv_perm, expert_slot, y, ks, stride, y_off, n_res, out)
-    if (y_bf16) SAEM_COMBINE(1, true);
-    else if (ks <= 1) SAEM_COMBINE(1, false);
-    else if (ks <= 2) SAEM_COMBINE(2, false);
-    else SAEM_COMBINE(16, false);
+#define SAEM_COMBINE(KS)                                                                                            \
+    hipLaunchKernelGGL((k_combine<kOutBf16, KS>), grid, dim3(256), 0, st, s.T, s.H, s.E, s.k, s.S, s.slots,      \
+                       topk_idx, topk_w, inv_perm, expert_slot, static_cast<const float*>(y), ks, stride, y_off,   \
+                       n_res, out)
+    if (y_bf16)
+        hipLaunchKernelGGL((k_combine_y16<kOutBf16>), dim3(s.T, (s.H + 2047) / 2048), dim3(256), 0, st, s.T, s.H,
+                           s.E, s.k, s.S, s.slots, topk_idx, topk_w, inv_perm, expert_slot,
+                           static_cast<const uint16_t*>(y), y_off, n_res, out);
+    else if (ks <= 1) SAEM_COMBINE(1);
+    else if (ks <= 2) SAEM_COMBINE(2);
+    else SAEM_COMBINE(16);
 #undef SAEM_COMBINE
     return hipGetLastError();
 }
