@@ -137,28 +137,28 @@ __device__ inline void topk_block(const float* s_lg, int rows, int E, int k, int
     __syncthreads();
 }
 
-// Router scores of tokens [t0, t0 + 16*TT) for all E experts, bf16 inputs, MFMA.
+// Router scores of tokens [t0, t0 + 16*TT) for all E experts on MFMA (bf16
+// inputs: 16x16x32; fp32 inputs: 16x16x4, two per 8-element fragment).
 // The 16 waves of the workgroup are TT token tiles x KP K parts (TT * KP = 16);
 // K part p takes the 32-wide K steps p, p + KP, p + 2 KP, ...  Partial tiles go
 // through `red` ([KP][16 TT][64] fp32) and are added in K-part order, so the
 // fp32 scores do not depend on timing.  Result: s_lg[row][e] = score + bias[e]
 // for row = t - t0 (rows of tokens >= T are left as garbage).
-template <int TT, int KP>
-__device__ void router_scores_bf16(int T, int H, int E, const uint16_t* __restrict__ x,
-                                   const uint16_t* __restrict__ wr, const float* __restrict__ bias, int t0,
-                                   float* s_lg, float* red) {
+template <typename Elt, int TT, int KP>
+__device__ void router_scores_mfma(int T, int H, int E, const Elt* __restrict__ x, const Elt* __restrict__ wr,
+                                   const float* __restrict__ bias, int t0, float* s_lg, float* red) {
     static_assert(TT * KP == kFrontWaves, "16 waves");
-    constexpr int U = 4;
+    constexpr int U = sizeof(Elt) == 2 ? 4 : 2;  // K steps per load batch (registers: 1024-thread workgroups)
     const int wave = threadIdx.x >> 6, lane = lane_id();
     const int r = lane & 15, kq = (lane >> 4) * 8;
     const int tt = wave % TT, kp = wave / TT;
     const int tok = t0 + 16 * tt + r;
-    const uint16_t* xp = (tok < T) ? x + (size_t)tok * H + kq : nullptr;
+    const Elt* xp = (tok < T) ? x + (size_t)tok * H + kq : nullptr;
     const int nsteps = H / 32;
     const int n_my = (nsteps > kp) ? (nsteps - kp + KP - 1) / KP : 0;
     for (int c0 = 0; c0 < E; c0 += kScoreChunk) {
         f32x4 acc[4];
-        const uint16_t* wp[4];
+        const Elt* wp[4];
         bool live[4];
 #pragma unroll
         for (int m = 0; m < 4; ++m) {
@@ -168,20 +168,20 @@ __device__ void router_scores_bf16(int T, int H, int E, const uint16_t* __restri
             wp[m] = (e < E) ? wr + (size_t)e * H + kq : nullptr;
         }
         for (int i = 0; i < n_my; i += U) {
-            bf16x8 A[U][4], B[U];
+            Frag8<Elt> A[U][4], B[U];
 #pragma unroll
             for (int u = 0; u < U; ++u) {
                 const int s = kp + KP * (i + u);
                 const bool ok = i + u < n_my;
-                B[u] = (ok && xp) ? load_bf16x8(xp + s * 32) : zero_bf16x8();
+                B[u] = (ok && xp) ? load_frag(xp + s * 32) : zero_frag<Elt>();
 #pragma unroll
-                for (int m = 0; m < 4; ++m) A[u][m] = (ok && wp[m]) ? load_bf16x8(wp[m] + s * 32) : zero_bf16x8();
+                for (int m = 0; m < 4; ++m) A[u][m] = (ok && wp[m]) ? load_frag(wp[m] + s * 32) : zero_frag<Elt>();
             }
 #pragma unroll
             for (int u = 0; u < U; ++u)
 #pragma unroll
                 for (int m = 0; m < 4; ++m)
-                    if (live[m]) acc[m] = mfma16x16x32(A[u][m], B[u], acc[m]);
+                    if (live[m]) acc[m] = mma_frag(A[u][m], B[u], acc[m]);
         }
         // lane holds experts 16m + 4(lane/16) + i of token row 16 tt + r
 #pragma unroll
@@ -199,20 +199,6 @@ __device__ void router_scores_bf16(int T, int H, int E, const uint16_t* __restri
         }
         __syncthreads();
     }
-}
-
-// fp32 inputs: one (token, expert) dot product per thread, plain fp32 FMA.
-__device__ inline void router_scores_f32(int T, int H, int E, const float* __restrict__ x,
-                                         const float* __restrict__ wr, const float* __restrict__ bias, int t0,
-                                         int rows, float* s_lg) {
-    for (int idx = threadIdx.x; idx < rows * E; idx += blockDim.x) {
-        const int row = idx / E, e = idx % E, t = t0 + row;
-        if (t >= T) continue;
-        float acc = 0.f;
-        for (int h = 0; h < H; ++h) acc = fmaf(x[(size_t)t * H + h], wr[(size_t)e * H + h], acc);
-        s_lg[row * kLgPitch + e] = acc + (bias ? bias[e] : 0.f);
-    }
-    __syncthreads();
 }
 
 // LDS ints the repack needs with NT threads.

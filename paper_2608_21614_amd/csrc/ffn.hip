@@ -12,8 +12,8 @@
 // MFMA A operands.
 //
 // Three kernel families:
-//  * stream  (T <= 64, decode; bf16 MFMA 16x16x32, fp32 MFMA 16x16x4): the
-//    weights are streamed from HBM exactly once.  A workgroup owns 32 features (phase 1: 32 gate + 32 up weight
+//  * stream  (T <= 64, decode, and fp32 prefill; bf16 MFMA 16x16x32, fp32 MFMA
+//    16x16x4): at decode the weights are streamed from HBM exactly once.  A workgroup owns 32 features (phase 1: 32 gate + 32 up weight
 //    rows) or 64 outputs (phase 2: 64 rows of W2) of one expert; the weights are
 //    the MFMA M side and the expert's tokens the N side, in tiles of 16.  Its
 //    four waves split K interleaved -- wave w takes the 32-wide K steps w, w+4,
@@ -29,7 +29,9 @@
 //    tile-layout blocks by direct global->LDS loads through a five-stage ring;
 //    a token gather first copies the resident groups' rows into that layout,
 //    and phase 1 writes the activations in it; the expert outputs are bf16.
-//  * f32     (fp32, T > 64): plain fp32 FMA, one output per thread.
+//    fp32 batches with T > 64 run the same kernel on chunks of 64 rows of a
+//    group: an item is then (group, weight rows, chunk), found from a prefix over
+//    the active groups that every workgroup computes.
 // All of them read counts and offsets from device memory: the grid is sized for
 // the worst case on the host and surplus workgroups exit at once.
 #include "common.hpp"
@@ -57,6 +59,7 @@ struct Args {
     int max_routed;   // routed groups the grid reserves (>= active resident experts)
     int ipg_r;        // items (workgroups) per routed group
     int ipg_s;        // items per shared group
+    int chunked;      // stream kernel: items cover the groups' rows in chunks of 64 (fp32 prefill)
     // offloaded-row pack done by the workgroups past the FFN items (phase 1 only)
     const float* topk_w;
     const int32_t* n_res;
@@ -171,8 +174,47 @@ __device__ __forceinline__ int group_token(const Args& a, const Group& g, int n)
     return (t >= 0 && t < a.T) ? t : -1;
 }
 
+constexpr int kGMaxGroups = 264;  // 256 routed + 8 shared
+
+// s_out[g] = sum_{g' < g} f(g') for g < n (n <= kGMaxGroups), s_out[n] = the total,
+// which is also returned; wave 0 scans, every thread of the workgroup must call.
+// *s_tot must not be read by any thread between its previous use and this call.
+template <typename Fn>
+__device__ int group_prefix(int n, int* s_out, int* s_tot, Fn f) {
+    if (threadIdx.x < 64) {
+        const int lane = threadIdx.x;
+        constexpr int PER = (kGMaxGroups + 63) / 64;
+        int v[PER], sum = 0;
+#pragma unroll
+        for (int i = 0; i < PER; ++i) {
+            const int gi = PER * lane + i;
+            v[i] = gi < n ? f(gi) : 0;
+            sum += v[i];
+        }
+        int inc = sum;
+#pragma unroll
+        for (int off = 1; off < 64; off <<= 1) {
+            const int o = __shfl_up(inc, off, 64);
+            if (lane >= off) inc += o;
+        }
+        int run = inc - sum;
+#pragma unroll
+        for (int i = 0; i < PER; ++i) {
+            const int gi = PER * lane + i;
+            if (gi < n) s_out[gi] = run;
+            run += v[i];
+        }
+        if (lane == 63) {
+            s_out[n] = inc;
+            *s_tot = inc;
+        }
+    }
+    __syncthreads();
+    return *s_tot;
+}
+
 // ---------------------------------------------------------------------------
-// stream kernel (decode)
+// stream kernel (decode, fp32 prefill)
 // ---------------------------------------------------------------------------
 
 // 16-row weight tiles per stream workgroup: two with a single token tile (twice
@@ -193,10 +235,12 @@ __global__ void __launch_bounds__(256) k_ffn_stream(Args a) {
     __shared__ int s_wsum[4];
     __shared__ int4 s_info[256];
     __shared__ f32x4 s_red[4][MT][NT][kWave];
+    __shared__ int s_ipre[kGMaxGroups + 1];
+    __shared__ int s_tot;
 
     const int item = blockIdx.x;
     const int n_items = a.max_routed * a.ipg_r + a.S * a.ipg_s;
-    if (!kDown && item >= n_items) {  // trailing workgroups pack the offloaded rows
+    if (!kDown && !a.chunked && item >= n_items) {  // trailing workgroups pack the offloaded rows
         pack_offloaded(a, item - n_items, gridDim.x - n_items, sizeof(Elt));
         return;
     }
@@ -204,8 +248,33 @@ __global__ void __launch_bounds__(256) k_ffn_stream(Args a) {
     // shared groups first: their items can be longer (Fs > F in phase 2), so they
     // start in the first wave of workgroups instead of forming a tail
     Group g;
-    int sub;
-    if (item < a.S * a.ipg_s) {
+    int sub, n0 = 0;  // n0: first row of the group this item covers
+    if (a.chunked) {
+        // group gi (the S shared groups, then the active routed ones) owns
+        // ipg x ceil(rows / 16 NT) items, the chunks of one weight slice adjacent
+        constexpr int kRows = 16 * NT;
+        auto rows_of = [&](int gi) { return gi < a.S ? a.T : max(s_info[gi - a.S].y, 0); };
+        const int total = group_prefix(a.S + nact, s_ipre, &s_tot, [&](int gi) {
+            return (gi < a.S ? a.ipg_s : a.ipg_r) * ((rows_of(gi) + kRows - 1) / kRows);
+        });
+        if (item >= total) return;
+        int lo = 0, hi = a.S + nact - 1;  // last group with s_ipre[gi] <= item
+        while (lo < hi) {
+            const int mid = (lo + hi + 1) >> 1;
+            if (s_ipre[mid] <= item) lo = mid;
+            else hi = mid - 1;
+        }
+        const int nch = (rows_of(lo) + kRows - 1) / kRows;
+        const int local = item - s_ipre[lo];
+        sub = local / nch;
+        n0 = (local % nch) * kRows;
+        if (lo < a.S) {
+            g = shared_group(a, lo, sizeof(Elt));
+        } else {
+            const int4 info = s_info[lo - a.S];
+            g = routed_group_of(a, info.x, info.y, info.z, sizeof(Elt));
+        }
+    } else if (item < a.S * a.ipg_s) {
         g = shared_group(a, item / a.ipg_s, sizeof(Elt));
         sub = item % a.ipg_s;
     } else {
@@ -267,12 +336,12 @@ __global__ void __launch_bounds__(256) k_ffn_stream(Args a) {
     if (nb > 0) load_w(A0, 0);
 
     // token operand rows (N side)
-    const int ntile = min(NT, (g.count + 15) / 16);
+    const int ntile = min(NT, (g.count - n0 + 15) / 16);
     const Elt* bp[NT];
 #pragma unroll
     for (int j = 0; j < NT; ++j) {
         bp[j] = nullptr;
-        const int n = 16 * j + r;
+        const int n = n0 + 16 * j + r;
         if (!kDown) {
             const int t = group_token(a, g, n);
             if (t >= 0) bp[j] = static_cast<const Elt*>(a.x) + (size_t)t * a.H + kq;
@@ -343,7 +412,7 @@ __global__ void __launch_bounds__(256) k_ffn_stream(Args a) {
             const int m = task / (NT * kWave);
             const int j = (task / kWave) % NT;
             const int l = task % kWave;
-            const int n = 16 * j + (l & 15);
+            const int n = n0 + 16 * j + (l & 15);
             if (j >= ntile || n >= g.count) continue;
             f32x4 gv = s_red[0][m][j][l], uv = s_red[0][m + MH][j][l];
 #pragma unroll
@@ -368,7 +437,7 @@ __global__ void __launch_bounds__(256) k_ffn_stream(Args a) {
             const int m = task / (NT * kWave);
             const int j = (task / kWave) % NT;
             const int l = task % kWave;
-            const int n = 16 * j + (l & 15);
+            const int n = n0 + 16 * j + (l & 15);
             if (j >= ntile || n >= g.count) continue;
             f32x4 v = s_red[0][m][j][l];
 #pragma unroll
@@ -424,7 +493,6 @@ constexpr int kGM = 256;          // weight rows per item
 constexpr int kGN = 256;          // group rows (tokens) per item
 constexpr int kGStages = 5;       // LDS ring
 constexpr int kGStageBytes = 32 * 1024;
-constexpr int kGMaxGroups = 264;  // 256 routed + 8 shared
 
 // One item of the tiled kernels (a single 32-byte scalar load).
 struct __attribute__((aligned(32))) TileItem {
@@ -466,42 +534,6 @@ __device__ __forceinline__ f32x16 mfma32x32x16(bf16x8 a, bf16x8 b, f32x16 c) {
     return __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, b, c, 0, 0, 0);
 }
 
-// s_out[g] = sum_{g' < g} f(g') for g < n (n <= kGMaxGroups), s_out[n] = the total,
-// which is also returned; wave 0 scans, every thread of the workgroup must call.
-// *s_tot must not be read by any thread between its previous use and this call.
-template <typename Fn>
-__device__ int group_prefix(int n, int* s_out, int* s_tot, Fn f) {
-    if (threadIdx.x < 64) {
-        const int lane = threadIdx.x;
-        constexpr int PER = (kGMaxGroups + 63) / 64;
-        int v[PER], sum = 0;
-#pragma unroll
-        for (int i = 0; i < PER; ++i) {
-            const int gi = PER * lane + i;
-            v[i] = gi < n ? f(gi) : 0;
-            sum += v[i];
-        }
-        int inc = sum;
-#pragma unroll
-        for (int off = 1; off < 64; off <<= 1) {
-            const int o = __shfl_up(inc, off, 64);
-            if (lane >= off) inc += o;
-        }
-        int run = inc - sum;
-#pragma unroll
-        for (int i = 0; i < PER; ++i) {
-            const int gi = PER * lane + i;
-            if (gi < n) s_out[gi] = run;
-            run += v[i];
-        }
-        if (lane == 63) {
-            s_out[n] = inc;
-            *s_tot = inc;
-        }
-    }
-    __syncthreads();
-    return *s_tot;
-}
 
 // Weight tiles of a group of width Fg: phase 1 covers 128 features per tile, phase 2 256 rows of W2.
 __device__ __forceinline__ int weight_tiles(const Args& a, int Fg, bool down) {
@@ -817,68 +849,6 @@ __global__ void __launch_bounds__(512, 1) k_ffn_tiled(Args a) {
     }
 }
 
-// ---------------------------------------------------------------------------
-// fp32 kernels
-// ---------------------------------------------------------------------------
-
-// Element (row, k) of a [R, K] matrix stored in the tile layout.
-__device__ __forceinline__ size_t tile_off(int row, int k, int K) {
-    return ((size_t)(row >> 4) * (K >> 5) + (k >> 5)) * 512 + ((k & 31) >> 3) * 128 + (row & 15) * 8 + (k & 7);
-}
-
-__device__ bool resolve_group_f32(const Args& a, int gidx, int* s_list, int* s_wsum, Group* g) {
-    const int nact = list_active(a, s_list, s_wsum);
-    if (gidx < a.max_routed) {
-        if (gidx >= nact) return false;
-        *g = routed_group(a, s_list[gidx], 4);
-    } else {
-        const int s = gidx - a.max_routed;
-        if (s >= a.S) return false;
-        *g = shared_group(a, s, 4);
-    }
-    return g->count > 0;
-}
-
-__global__ void __launch_bounds__(256) k_ffn1_f32(Args a) {
-    __shared__ int s_list[256];
-    __shared__ int s_wsum[4];
-    Group g;
-    if (!resolve_group_f32(a, blockIdx.x, s_list, s_wsum, &g)) return;
-    const int f = blockIdx.y * 64 + (threadIdx.x & 63);
-    if (f >= g.Fg) return;
-    const float* x = static_cast<const float*>(a.x);
-    const float* w13 = reinterpret_cast<const float*>(g.w13);
-    float* act = static_cast<float*>(a.act);
-    for (int n = threadIdx.x >> 6; n < g.count; n += 4) {
-        const int t = group_token(a, g, n);
-        if (t < 0) continue;
-        const float* xr = x + (size_t)t * a.H;
-        float gs = 0.f, us = 0.f;
-        for (int h = 0; h < a.H; ++h) {
-            gs = fmaf(xr[h], w13[tile_off(f, h, a.H)], gs);
-            us = fmaf(xr[h], w13[tile_off(g.Fg + f, h, a.H)], us);
-        }
-        act[(size_t)(g.rowbase + n) * a.Fa + f] = silu(gs) * us;
-    }
-}
-
-__global__ void __launch_bounds__(256) k_ffn2_f32(Args a) {
-    __shared__ int s_list[256];
-    __shared__ int s_wsum[4];
-    Group g;
-    if (!resolve_group_f32(a, blockIdx.x, s_list, s_wsum, &g)) return;
-    const int h = blockIdx.y * 64 + (threadIdx.x & 63);
-    if (h >= a.H) return;
-    const float* w2 = reinterpret_cast<const float*>(g.w2);
-    const float* act = static_cast<const float*>(a.act);
-    for (int n = threadIdx.x >> 6; n < g.count; n += 4) {
-        const float* ar = act + (size_t)(g.rowbase + n) * a.Fa;
-        float s = 0.f;
-        for (int f = 0; f < g.Fg; ++f) s = fmaf(ar[f], w2[tile_off(h, f, g.Fg)], s);
-        a.y[(size_t)(g.rowbase + n) * a.H + h] = s;
-    }
-}
-
 // y_out[p] = sum_c y[c][p] for resident packed rows p < n_res and all shared rows
 // (kInBf16: a single chunk of bf16 rows, widened).
 template <bool kInBf16>
@@ -986,6 +956,7 @@ Args make_args(const Shape& s, const FfnArgs& fa) {
     a.act = fa.act; a.Fa = fa.Fa; a.y = fa.y; a.ks = fa.ks; a.y_ks_stride = fa.y_ks_stride;
     a.max_routed = max_routed_groups(s);
     a.ipg_r = a.ipg_s = 0;
+    a.chunked = 0;
     a.topk_w = fa.topk_w;
     a.n_res = fa.n_res;
     a.off_rows = fa.off_rows;
@@ -1055,14 +1026,21 @@ hipError_t launch_grouped_ffn(const Shape& s, const FfnArgs& fa, hipStream_t st,
         return e;
     };
     Args a = make_args(s, fa);
-    if (!s.bf16 && !use_stream(s)) {  // fp32 prefill: plain FMA kernels
-        a.ipg_r = a.ipg_s = 1;
-        const int groups = a.max_routed + s.S;
-        if (groups == 0) return hipSuccess;
-        const int fmax = s.S > 0 && s.Fs > s.F ? s.Fs : s.F;
-        hipLaunchKernelGGL(k_ffn1_f32, dim3(groups, fmax / 64), dim3(256), 0, st, a);
+    if (!s.bf16 && !use_stream(s)) {
+        // fp32 prefill: the stream kernel over chunks of 64 rows; a workgroup per
+        // worst-case item: the routed groups hold at most ceil(P / 64) full chunks
+        // plus one partial chunk each
+        a.chunked = 1;
+        const long long chunks_r = a.max_routed == 0 ? 0 : ((long long)s.T * s.k + 63) / 64 + a.max_routed;
+        const long long chunks_s = (long long)s.S * ((s.T + 63) / 64);
+        a.ipg_r = s.F / 32;
+        a.ipg_s = s.S > 0 ? s.Fs / 32 : 1;
+        long long grid = a.ipg_r * chunks_r + a.ipg_s * chunks_s;
+        if (grid > 0) hipLaunchKernelGGL((k_ffn_stream<float, 4, false, false>), dim3((unsigned)grid), dim3(256), 0, st, a);
         if (hipError_t e = mark(); e != hipSuccess) return e;
-        hipLaunchKernelGGL(k_ffn2_f32, dim3(groups, s.H / 64), dim3(256), 0, st, a);
+        a.ipg_r = a.ipg_s = s.H / 64;
+        grid = a.ipg_r * (chunks_r + chunks_s);
+        if (grid > 0) hipLaunchKernelGGL((k_ffn_stream<float, 4, true, false>), dim3((unsigned)grid), dim3(256), 0, st, a);
         return hipGetLastError();
     }
     if (use_stream(s)) {

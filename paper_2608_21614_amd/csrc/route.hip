@@ -1,8 +1,8 @@
 // route.hip -- router scores and top-k gate (SAEM Section II-A: top-k gating by
 // a router), and the decode front end (scores + top-k + repacking).
 //
-// Scores run on MFMA (v_mfma_f32_16x16x32_bf16): router rows are the M side,
-// 16 tokens the N side.
+// Scores run on MFMA (v_mfma_f32_16x16x32_bf16, or v_mfma_f32_16x16x4_f32 for
+// fp32 inputs): router rows are the M side, 16 tokens the N side.
 //
 //  * T > 64 (prefill): k_route_topk, 16 tokens per 1024-thread workgroup whose
 //    16 waves split K and add their partial tiles in a fixed order.
@@ -31,11 +31,11 @@ __global__ void __launch_bounds__(kFrontThreads)
     const int t0 = blockIdx.x * 16;
     if (!logits_in) {
         if (kBf16)
-            router_scores_bf16<1, kFrontWaves>(T, H, E, static_cast<const uint16_t*>(x),
-                                               static_cast<const uint16_t*>(wr), bias, t0, s_lg, s_red);
+            router_scores_mfma<uint16_t, 1, kFrontWaves>(T, H, E, static_cast<const uint16_t*>(x),
+                                                         static_cast<const uint16_t*>(wr), bias, t0, s_lg, s_red);
         else
-            router_scores_f32(T, H, E, static_cast<const float*>(x), static_cast<const float*>(wr), bias, t0, 16,
-                              s_lg);
+            router_scores_mfma<float, 1, kFrontWaves>(T, H, E, static_cast<const float*>(x),
+                                                      static_cast<const float*>(wr), bias, t0, s_lg, s_red);
     }
     const int rows = min(16, T - t0);
     // scores <-> global, coalesced

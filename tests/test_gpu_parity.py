@@ -119,7 +119,7 @@ def test_route_topk_given_scores_bit_exact(moe, T, E, k):
 @pytest.mark.parametrize("dtype,T,H,E,k,bias", [
     ("bf16", 1, 64, 8, 2, "none"), ("bf16", 17, 256, 60, 4, "zipf"), ("bf16", 100, 2048, 64, 6, "zipf"),
     ("bf16", 33, 4096, 8, 2, "none"), ("bf16", 16, 128, 256, 8, "zipf"), ("f32", 16, 256, 8, 2, "none"),
-    ("f32", 21, 64, 130, 5, "zipf"),
+    ("f32", 21, 64, 130, 5, "zipf"), ("f32", 100, 256, 64, 6, "zipf"),
 ])
 def test_route_topk_computed_scores(moe, dtype, T, H, E, k, bias):
     say("route computed", dtype, T, H, E, k, bias)
@@ -400,6 +400,10 @@ EDGE = [
     (40, 128, 256, 64, 8, 8, 64, "bf16", 256),
     (200, 128, 256, 64, 8, 8, 128, "bf16", 128),
     (24, 64, 16, 64, 8, 8, 64, "f32", 8),
+    # fp32 prefill on MFMA: groups of several 64-row chunks (one ragged), shared
+    # experts wider than the routed ones, and more experts than resident slots
+    (300, 256, 16, 192, 4, 2, 320, "f32", 10),
+    (65, 128, 4, 64, 1, 1, 64, "f32", 4),
 ]
 
 

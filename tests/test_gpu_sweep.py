@@ -3,7 +3,7 @@ the oracle (routing, repack and the resident partial output; the same checks as
 the fixed edge cases, over shape combinations those do not list).
 
 The shapes cover both FFN paths (T <= 64: streaming kernel; T > 64: tiled kernel
-for bf16, plain kernels for fp32), 0-2 shared experts, partial, empty and full
+for bf16, the streaming kernel over 64-row chunks for fp32), 0-2 shared experts, partial, empty and full
 residency, k up to min(E, 8), and widths that leave ragged tiles."""
 from __future__ import annotations
 
