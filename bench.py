@@ -39,6 +39,7 @@ sys.path.insert(0, ROOT)
 
 HBM_PEAK_GBPS = 8000.0          # MI355X HBM3E, 8 TB/s
 MFMA_BF16_PEAK_TFLOPS = 2500.0  # dense bf16
+MFMA_F32_PEAK_TFLOPS = 157.3    # dense fp32
 METRIC = "MoE-layer tokens/sec + achieved HBM GB/s (expert weights) at decode batch"
 TRAFFIC_DIR = os.path.join(ROOT, "profiles")
 KERNEL_SOURCES = [os.path.join(ROOT, "paper_2608_21614_amd", "csrc", n) for n in ("ffn.hip", "common.hpp")]
@@ -92,11 +93,16 @@ def algorithmic_bytes(cfg, counts, resident):
                 layer_bytes=layer, flops=flops, phase1_flops=4 * H * F * n_res + cfg.shared * 4 * H * cfg.shared_ffn * T)
 
 
-def layer_roofline(alg, ms_per_step: float):
+def mfma_peak_tflops(dtype: str) -> float:
+    """Dense MFMA peak of the layer's arithmetic type."""
+    return MFMA_BF16_PEAK_TFLOPS if dtype == "bf16" else MFMA_F32_PEAK_TFLOPS
+
+
+def layer_roofline(alg, ms_per_step: float, dtype: str = "bf16"):
     """The whole layer against its roofline: the slower of moving its algorithmic bytes at the HBM
-    peak and doing its algorithmic flops at the dense bf16 MFMA peak."""
+    peak and doing its algorithmic flops at the dense MFMA peak of its type (bf16 or fp32)."""
     t_bytes = alg["layer_bytes"] / (HBM_PEAK_GBPS * 1e9)
-    t_flops = alg["flops"] / (MFMA_BF16_PEAK_TFLOPS * 1e12)
+    t_flops = alg["flops"] / (mfma_peak_tflops(dtype) * 1e12)
     t_roof = max(t_bytes, t_flops)
     return {"t_roof_us": t_roof * 1e6, "t_bytes_us": t_bytes * 1e6, "t_flops_us": t_flops * 1e6,
             "bound": "hbm" if t_bytes >= t_flops else "mfma", "frac": t_roof / (ms_per_step * 1e-3)}
@@ -316,7 +322,8 @@ def trace_timings(seed: int, lags, detect: bool = False, persistence: float = 0.
 # roofline and a bounded CPU-oracle sample): the tiny fp32 layer, the shared+routed
 # decode batch, the prefill chunk, one layer call of the stage-structured trace, and
 # the Qwen3-MoE-like decode batch
-OTHER_WORKLOADS = ["c1_tiny_f32", "c3_shared_decode", "c4_prefill", "c5_stage_trace", "c6_qwen3_decode"]
+OTHER_WORKLOADS = ["c1_tiny_f32", "c3_shared_decode", "c4_prefill", "c5_stage_trace", "c6_qwen3_decode",
+                   "c4_prefill_f32"]
 
 
 def measure_workload(name, cfg, args, steps: int, warmup: int, cpu_seconds: float, primary: bool,
@@ -467,12 +474,16 @@ def measure_workload(name, cfg, args, steps: int, warmup: int, cpu_seconds: floa
     p1_s = p1_us * 1e-6
     traffic = read_traffic(name)
     if cfg.tokens > 64:
-        # prefill-size batches run the tiled MFMA kernels, at the ridge: FLOP rate
-        # against the dense bf16 matrix-core peak, and the HBM fraction beside it
+        # prefill-size batches run MFMA kernels at the ridge (bf16: the tiled kernel; fp32: the
+        # stream kernel over 64-row chunks): FLOP rate against the dense matrix-core peak of the
+        # layer's type, and the HBM fraction beside it
         achieved = alg["phase1_flops"] / p1_s / 1e12
-        roofline = {"kernel": "k_ffn_tiled (phase 1: gate/up projections + SwiGLU)", "bound": "mfma",
-                    "achieved": achieved, "peak": MFMA_BF16_PEAK_TFLOPS, "unit": "TFLOP/s",
-                    "frac": achieved / MFMA_BF16_PEAK_TFLOPS, "traffic": traffic,
+        peak = mfma_peak_tflops(cfg.dtype)
+        kname = ("k_ffn_tiled (phase 1: gate/up projections + SwiGLU)" if cfg.dtype == "bf16" else
+                 "k_ffn_stream fp32, 64-row chunks (phase 1: gate/up projections + SwiGLU)")
+        roofline = {"kernel": kname, "bound": "mfma",
+                    "achieved": achieved, "peak": peak, "unit": "TFLOP/s",
+                    "frac": achieved / peak, "traffic": traffic,
                     "algorithmic_flops_per_launch": alg["phase1_flops"],
                     "algorithmic_bytes_per_launch": alg["phase1_bytes"],
                     "hbm_frac_algorithmic": alg["phase1_bytes"] / p1_s / 1e9 / HBM_PEAK_GBPS, "mean_launch_us": p1_us,
@@ -505,7 +516,7 @@ def measure_workload(name, cfg, args, steps: int, warmup: int, cpu_seconds: floa
         "ms_per_step_without_events": ms_no_events,
         # whole layer against its roofline: the slower of moving its algorithmic bytes at
         # the HBM peak and doing its algorithmic flops at the dense bf16 MFMA peak
-        "layer_roofline": layer_roofline(alg, ms_per_step),
+        "layer_roofline": layer_roofline(alg, ms_per_step, cfg.dtype),
         "roofline": roofline,
         "hbm_read_probe_GBps": read_probe_gbps,
     }

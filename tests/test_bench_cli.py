@@ -73,6 +73,12 @@ def test_committed_traffic_matches_the_current_kernels(workload):
     assert bench.read_traffic(workload) is not None, f"profiles/traffic_ffn_phase1_{workload}.txt is stale or missing"
 
 
+def test_layer_roofline_takes_the_fp32_peak_for_fp32_layers():
+    alg = {"layer_bytes": 8e12 * 10e-6, "flops": 157.3e12 * 50e-6}   # 10 us of bytes, 50 us of fp32 flops
+    r = bench.layer_roofline(alg, ms_per_step=0.1, dtype="f32")
+    assert r["bound"] == "mfma" and abs(r["t_roof_us"] - 50.0) < 1e-9 and abs(r["frac"] - 0.5) < 1e-12
+
+
 def test_layer_roofline_bound_and_fraction():
     alg = {"layer_bytes": 8e12 * 100e-6, "flops": 2.5e15 * 40e-6}     # 100 us of bytes, 40 us of flops
     r = bench.layer_roofline(alg, ms_per_step=0.2)

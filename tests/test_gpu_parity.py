@@ -357,6 +357,15 @@ def test_layer_c4_prefill(moe, seed):
     check_ffn_rows(moe, dev, lay, ref)
 
 
+def test_layer_c4_prefill_f32(moe):
+    """The prefill shape in fp32 (the fp32 MFMA path at full size): every token's output at
+    the fp32 bar, and every FFN row."""
+    say("layer c4_prefill_f32 seed 0 (all 2048 tokens, all FFN rows)")
+    lay = SyntheticLayer(CONFIGS["c4_prefill_f32"], 0)
+    dev, _, ref = run_and_check_layer(moe, lay)
+    check_ffn_rows(moe, dev, lay, ref)
+
+
 @pytest.mark.parametrize("name", ["c2_mixtral_decode", "c3_shared_decode"])
 def test_ffn_rows_decode(moe, name):
     """Decode configs: every resident packed row and shared row of the grouped FFN (split-K sums added)."""

@@ -138,6 +138,11 @@ CONFIGS: Dict[str, MoEConfig] = {
         "c4_prefill", "bf16", tokens=2048, hidden=2048, experts=64, ffn=1408, top_k=6,
         shared=2, shared_ffn=1408, n_resident=48, residency="zipf_top", bias="zipf",
         description="bf16 prefill chunk of 2048 tokens, H 2048, 64 routed F 1408 top-6 + 2 shared F 1408, 48/64 resident, Zipf(1.1)"),
+    # the prefill shape in fp32: the fp32 path (MFMA 16x16x4) at prefill size
+    "c4_prefill_f32": MoEConfig(
+        "c4_prefill_f32", "f32", tokens=2048, hidden=2048, experts=64, ffn=1408, top_k=6,
+        shared=2, shared_ffn=1408, n_resident=48, residency="zipf_top", bias="zipf",
+        description="fp32 prefill chunk of 2048 tokens, H 2048, 64 routed F 1408 top-6 + 2 shared F 1408, 48/64 resident, Zipf(1.1)"),
     # many small experts with a wide top-k (the Qwen3-MoE family the paper evaluates): the
     # shape of the bookkeeping A/B, where per-expert launches cost the most
     "c6_qwen3_decode": MoEConfig(
