@@ -666,18 +666,25 @@ __global__ void __launch_bounds__(256) k_gather_tokens(Args a, int blocks_max) {
     }
 }
 
+// One workgroup per CU (the kernel's LDS admits one), looping over items.  tab: this
+// phase's item table, passed on its own and restrict-qualified, so that the compiler knows
+// the kernel's stores leave it alone and reads the descriptors through scalar loads (a
+// vector load would come with a wait for every outstanding memory operation).
 template <bool kDown>
-__global__ void __launch_bounds__(512, 1) k_ffn_tiled(Args a) {
+__global__ void __launch_bounds__(512, 1) k_ffn_tiled(Args a, const TileItem* __restrict__ tab) {
     __shared__ __attribute__((aligned(1024))) uint8_t sbuf[kGStages * kGStageBytes];
 
+    // XCD-aware order: XCD x = pid % 8 takes the real items [x per, (x + 1) per), which its
+    // workgroups take in turn: the CUs of an XCD start each round together on neighbouring
+    // tiles of one group and share its panels in their L2
     const int n_items = a.tmeta[kDown ? 1 : 0];
-    // XCD-aware order: XCD x = pid % 8 takes the real items [x per, (x + 1) per)
     const int per = (n_items + 7) / 8;
-    const int j = blockIdx.x / 8;
-    if (j >= per) return;
-    const int item = (blockIdx.x % 8) * per + j;
-    if (item >= n_items) return;
-    const TileItem it = reinterpret_cast<const TileItem*>(a.tmeta + 8)[(kDown ? a.tcap1 : 0) + item];
+    const int xcd = blockIdx.x % 8;
+    const int xend = min((xcd + 1) * per, n_items);
+    const int step = gridDim.x / 8;
+    for (int item = xcd * per + (int)(blockIdx.x / 8); item < xend; item += step) {
+    __syncthreads();  // the previous item's epilogue is done with the LDS
+    const TileItem it = tab[item];
 
     const int tid = threadIdx.x, lane = lane_id();
     const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
@@ -846,6 +853,7 @@ __global__ void __launch_bounds__(512, 1) k_ffn_tiled(Args a) {
             const u32x4 v = *reinterpret_cast<const u32x4*>(sy + nl * kPitch + 8 * piece);
             *reinterpret_cast<u32x4*>(a.y16 + (size_t)(it.rowbase + n0 + nl) * a.H + h) = v;
         }
+    }
     }
 }
 
@@ -1070,18 +1078,26 @@ hipError_t launch_grouped_ffn(const Shape& s, const FfnArgs& fa, hipStream_t st,
         }
         return hipGetLastError();
     }
-    // tiled: a workgroup per worst-case item (the table the token gather wrote holds the
-    // real ones, which the kernel maps over the XCDs); the offloaded rows were packed
-    // by the token gather
-    auto round8 = [](long long n) { return (n + 7) / 8 * 8; };
+    // tiled: one workgroup per CU, each taking its XCD's items from the table the token
+    // gather wrote in turn; the offloaded rows were packed by the token gather
+    int dev = 0, cus = 0;
+    if (hipError_t e = hipGetDevice(&dev); e != hipSuccess) return e;
+    if (hipError_t e = hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev); e != hipSuccess)
+        return e;
+    const long long wgs = cus < 8 ? 8 : cus / 8 * 8;
+    auto tiled_grid = [&](long long items) { return items < wgs ? (items + 7) / 8 * 8 : wgs; };
     {
-        const long long grid = round8(tiled_items(s, false));
-        if (grid > 0) hipLaunchKernelGGL((k_ffn_tiled<false>), dim3((unsigned)grid), dim3(512), 0, st, a);
+        const long long grid = tiled_grid(tiled_items(s, false));
+        if (grid > 0)
+            hipLaunchKernelGGL((k_ffn_tiled<false>), dim3((unsigned)grid), dim3(512), 0, st, a,
+                               reinterpret_cast<const TileItem*>(a.tmeta + 8));
     }
     if (hipError_t e = mark(); e != hipSuccess) return e;
     {
-        const long long grid = round8(tiled_items(s, true));
-        if (grid > 0) hipLaunchKernelGGL((k_ffn_tiled<true>), dim3((unsigned)grid), dim3(512), 0, st, a);
+        const long long grid = tiled_grid(tiled_items(s, true));
+        if (grid > 0)
+            hipLaunchKernelGGL((k_ffn_tiled<true>), dim3((unsigned)grid), dim3(512), 0, st, a,
+                               reinterpret_cast<const TileItem*>(a.tmeta + 8) + a.tcap1);
     }
     return hipGetLastError();
 }
