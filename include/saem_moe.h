@@ -278,6 +278,8 @@ moe_status moe_stage_plan(int32_t experts, int32_t slots, const int64_t* log, co
 
 /* flags of moe_host_ffn */
 #define MOE_HOST_PIN 1u    /* pin the worker threads to the calling thread's CPUs on one NUMA node */
+#define MOE_HOST_NO_BF16_DOT 2u  /* bf16 layers: widen to fp32 in phase 1 even where the CPU has the
+                                    AVX-512 bf16 dot-product instruction (used by default there) */
 
 /*
  * In-situ host execution of the offloaded experts (Section IV-D.1, IV-D.2):
@@ -298,7 +300,11 @@ moe_status moe_stage_plan(int32_t experts, int32_t slots, const int64_t* log, co
  *                      offloaded rows (moe_repack / moe_layer_forward off_rows)
  *   y_off              [T*k - n_res, H] fp32 out: y_off[r] = SwiGLU_e(off_rows[r])
  *                      for the expert e that owns packed row n_res + r
- * fp32 accumulation; A = silu(x W1) * (x W3) is kept in fp32.  Returns
+ * fp32 accumulation; A = silu(x W1) * (x W3) is kept in fp32.  For bf16 layers
+ * on a CPU with the AVX-512 bf16 dot-product instruction, x W1 and x W3 use it
+ * (each bf16 product exact in fp32, pairs added into fp32 accumulators; inputs
+ * below the fp32 normal range count as zero) unless flags has
+ * MOE_HOST_NO_BF16_DOT.  Returns
  * MOE_ERR_INVALID_ARG if the offloaded segments do not tile [n_res, T*k) or a
  * needed pointer is NULL; nothing is written then.
  */

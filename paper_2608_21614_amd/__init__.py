@@ -23,6 +23,7 @@ MOE_F32, MOE_BF16 = 0, 1
 MOE_LOGITS_IN = 1
 MOE_STAGE_EVENTS = 7
 MOE_HOST_PIN = 1
+MOE_HOST_NO_BF16_DOT = 2
 
 EXPORTED = [
     "moe_abi_version", "moe_status_str", "moe_check_dims", "moe_workspace_bytes", "moe_route_topk",
@@ -238,13 +239,14 @@ def moe_read_probe(src, sink, nbytes=None, stream=None):
 
 
 def moe_host_ffn(dims, counts, seg_start, n_res: int, w13_host, w2_host, off_rows, y_off=None, threads: int = 0,
-                 pin: bool = False):
+                 pin: bool = False, bf16_dot: bool = True):
     """Host execution of the offloaded experts (host numpy arrays only).
 
     counts, seg_start: int32 [E]; w13_host[e] / w2_host[e]: row-major [2F, H] / [H, F]
     arrays of the layer dtype (uint16 bf16 bits or float32) for the experts with
     offloaded rows, None for the others; off_rows: [T*k - n_res, H].  Returns
-    y_off [T*k - n_res, H] float32 (written into `y_off` when given).
+    y_off [T*k - n_res, H] float32 (written into `y_off` when given).  bf16_dot=False keeps
+    bf16 layers on the widened fp32 dot products where the CPU has bf16 ones.
     """
     import numpy as np
     E, H = dims.experts, dims.hidden
@@ -267,7 +269,8 @@ def moe_host_ffn(dims, counts, seg_start, n_res: int, w13_host, w2_host, off_row
     _check(lib.moe_host_ffn(ctypes.byref(dims), cnt.ctypes.data, seg.ctypes.data, int(n_res), p13, p2,
                             rows.ctypes.data if rows is not None else None,
                             y_off.ctypes.data if n_off > 0 else None, int(threads),
-                            MOE_HOST_PIN if pin else 0), "moe_host_ffn")
+                            (MOE_HOST_PIN if pin else 0) | (0 if bf16_dot else MOE_HOST_NO_BF16_DOT)),
+           "moe_host_ffn")
     return y_off
 
 

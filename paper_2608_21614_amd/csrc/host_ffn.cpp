@@ -9,11 +9,14 @@
 //   A_e = silu(X_e W1_e) * (X_e W3_e)      [c_e, F]   fp32
 //   Y_e = A_e W2_e                          [c_e, H]   fp32 -> y_off rows
 // A work item is 64 output features of one expert; it walks K in 512-wide
-// slices so that the slice of (up to) 8 fp32 token rows stays in L1 while the
+// slices so that the slice of (up to) 8 token rows stays in L1 while the
 // item's 64 weight rows stream past it: every weight element is read from
 // memory once per block of 8 rows (from L2 for later blocks), so the work is
 // bound by host memory bandwidth on the expert weights, as the device FFN is
-// by HBM.
+// by HBM.  Dot products: AVX2 FMAs on fp32 (bf16 widened); for bf16 layers on a
+// CPU with the AVX-512 bf16 dot-product instruction, phase 1 (bf16 token rows
+// times bf16 weights) uses it instead: 32 products per instruction, each exact
+// in fp32, added in pairs into fp32 accumulators.
 #include <errno.h>
 #include <immintrin.h>
 #include <pthread.h>
@@ -84,6 +87,50 @@ __attribute__((target("avx2,fma"))) void block_dot_avx2(const void* w, size_t ld
             s = _mm_add_ss(s, _mm_shuffle_ps(s, s, 0x55));
             sums[f * kRowBlock + r] += _mm_cvtss_f32(s);
         }
+    }
+}
+
+// The same over bf16 token rows x (elements), bf16 weights, with vdpbf16ps: every
+// product of two bf16 values is exact in fp32; pairs of products are added into the
+// fp32 accumulators.  The instruction treats inputs below the fp32 normal range as
+// zero and flushes such results to zero.  klen % 32 == 0.
+template <int R>
+__attribute__((target("avx512f,avx512bw,avx512bf16"))) void block_dot_bf16dp(const void* w, size_t ldw,
+                                                                           const uint16_t* x, size_t ldx,
+                                                                           int klen, int nf, float* sums) {
+    for (int f = 0; f < nf; ++f) {
+        const uint16_t* wr = static_cast<const uint16_t*>(w) + f * ldw;
+        __m512 acc[R];
+        for (int r = 0; r < R; ++r) acc[r] = _mm512_setzero_ps();
+        for (int k = 0; k < klen; k += 32) {
+            const __m512bh wv = (__m512bh)_mm512_loadu_si512(wr + k);
+            for (int r = 0; r < R; ++r)
+                acc[r] = _mm512_dpbf16_ps(acc[r], wv, (__m512bh)_mm512_loadu_si512(x + (size_t)r * ldx + k));
+        }
+        for (int r = 0; r < R; ++r) sums[f * kRowBlock + r] += _mm512_reduce_add_ps(acc[r]);
+    }
+}
+
+using BlockDotBf16 = void (*)(const void*, size_t, const uint16_t*, size_t, int, int, float*);
+
+BlockDotBf16 pick_rows_bf16dp(int R) {
+#define SAEM_ROWS(n) \
+    case n: return block_dot_bf16dp<n>;
+    switch (R) {
+        SAEM_ROWS(1) SAEM_ROWS(2) SAEM_ROWS(3) SAEM_ROWS(4) SAEM_ROWS(5) SAEM_ROWS(6) SAEM_ROWS(7)
+        default: return block_dot_bf16dp<8>;
+    }
+#undef SAEM_ROWS
+}
+
+// rows_times_weights for bf16 token rows and bf16 weights on the dot-product instruction.
+void rows_times_weights_bf16dp(const void* w, size_t ldw, int K, int nf, const uint16_t* x, size_t ldx, int R,
+                               float* out) {
+    const BlockDotBf16 fn = pick_rows_bf16dp(R);
+    for (int i = 0; i < nf * kRowBlock; ++i) out[i] = 0.f;
+    for (int k0 = 0; k0 < K; k0 += kKBlock) {
+        const int klen = std::min(kKBlock, K - k0);
+        fn(static_cast<const uint16_t*>(w) + k0, ldw, x + k0, ldx, klen, nf, out);
     }
 }
 
@@ -200,7 +247,8 @@ moe_status moe_host_ffn(const moe_dims* dims, const int32_t* counts, const int32
                         const void* const* w13, const void* const* w2, const void* off_rows, float* y_off,
                         int32_t threads, uint32_t flags) {
     if (moe_status st = moe_check_dims(dims); st != MOE_OK) return st;
-    if (!counts || !seg_start || !w13 || !w2 || (flags & ~MOE_HOST_PIN)) return MOE_ERR_INVALID_ARG;
+    if (!counts || !seg_start || !w13 || !w2 || (flags & ~(MOE_HOST_PIN | MOE_HOST_NO_BF16_DOT)))
+        return MOE_ERR_INVALID_ARG;
     const int T = dims->tokens, H = dims->hidden, E = dims->experts, F = dims->ffn, k = dims->top_k;
     const int P = T * k;
     if (n_res < 0 || n_res > P) return MOE_ERR_INVALID_ARG;
@@ -231,10 +279,15 @@ moe_status moe_host_ffn(const moe_dims* dims, const int32_t* counts, const int32
     if (flags & MOE_HOST_PIN) cpus = local_cpus();
     if (!cpus.empty() && threads <= 0) nthreads = (int)cpus.size();
 
-    // packed rows in fp32
-    std::vector<float> xf((size_t)n_off * H), act((size_t)n_off * F);
-    for (size_t i = 0; i < (size_t)n_off * H; ++i)
-        xf[i] = bf16 ? bf16_bits_to_f32(static_cast<const uint16_t*>(off_rows)[i]) : static_cast<const float*>(off_rows)[i];
+    // phase 1 on the bf16 dot-product instruction where the CPU has it (bf16 rows as they
+    // are), else on fp32 rows
+    static const bool cpu_bf16dp = __builtin_cpu_supports("avx512bf16");
+    const bool bf16dp = bf16 && cpu_bf16dp && !(flags & MOE_HOST_NO_BF16_DOT);
+    const uint16_t* xb = static_cast<const uint16_t*>(off_rows);
+    std::vector<float> xf(bf16dp ? 0 : (size_t)n_off * H), act((size_t)n_off * F);
+    if (!bf16dp)
+        for (size_t i = 0; i < (size_t)n_off * H; ++i)
+            xf[i] = bf16 ? bf16_bits_to_f32(xb[i]) : static_cast<const float*>(off_rows)[i];
 
     // work items: (job, block of kChunk output features); inside an item every
     // weight row is applied to all of the expert's rows, kRowBlock at a time,
@@ -259,9 +312,15 @@ moe_status moe_host_ffn(const moe_dims* dims, const int32_t* counts, const int32
         float g[kChunk * kRowBlock], u[kChunk * kRowBlock];
         for (int r0 = 0; r0 < jb.rows; r0 += kRowBlock) {
             const int R = std::min(kRowBlock, jb.rows - r0);
-            const float* x = xf.data() + (size_t)(jb.row0 + r0) * H;
-            rows_times_weights(bf16, w + (size_t)it.f0 * H * elt, H, H, nf, x, H, R, g);
-            rows_times_weights(bf16, w + (size_t)(F + it.f0) * H * elt, H, H, nf, x, H, R, u);
+            if (bf16dp) {
+                const uint16_t* x = xb + (size_t)(jb.row0 + r0) * H;
+                rows_times_weights_bf16dp(w + (size_t)it.f0 * H * elt, H, H, nf, x, H, R, g);
+                rows_times_weights_bf16dp(w + (size_t)(F + it.f0) * H * elt, H, H, nf, x, H, R, u);
+            } else {
+                const float* x = xf.data() + (size_t)(jb.row0 + r0) * H;
+                rows_times_weights(bf16, w + (size_t)it.f0 * H * elt, H, H, nf, x, H, R, g);
+                rows_times_weights(bf16, w + (size_t)(F + it.f0) * H * elt, H, H, nf, x, H, R, u);
+            }
             for (int f = 0; f < nf; ++f)
                 for (int r = 0; r < R; ++r) {
                     const float gv = g[f * kRowBlock + r], uv = u[f * kRowBlock + r];

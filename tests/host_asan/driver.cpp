@@ -105,10 +105,11 @@ static int host_ffn(std::mt19937& rng) {
         std::vector<uint8_t> rows;
         fill(rows, (size_t)P * H, 1.f);
         std::vector<float> y((size_t)P * H, -1.f);
-        for (int threads : {1, 3, 0}) {
-            if (moe_host_ffn(&d, counts, seg, 0, p13.data(), p2.data(), rows.data(), y.data(), threads, 0) != MOE_OK)
-                return fail("host ffn");
-        }
+        for (int threads : {1, 3, 0})
+            for (uint32_t flags : {0u, (uint32_t)MOE_HOST_NO_BF16_DOT})  // bf16 dot products where the CPU has them, and widened
+                if (moe_host_ffn(&d, counts, seg, 0, p13.data(), p2.data(), rows.data(), y.data(), threads, flags) !=
+                    MOE_OK)
+                    return fail("host ffn");
         for (float v : y)
             if (v == -1.f || v != v) return fail("host ffn left a row unwritten");
         const int32_t bad_seg[E] = {0, 3, 4, 8};  // segments do not tile [0, P)

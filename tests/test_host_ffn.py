@@ -62,14 +62,23 @@ SMALL = [
 ]
 
 
+def cpu_has_bf16_dot() -> bool:
+    try:
+        with open("/proc/cpuinfo") as f:
+            return "avx512_bf16" in f.read()
+    except OSError:
+        return False
+
+
 @pytest.mark.parametrize("name,dtype,T,H,E,F,k", SMALL, ids=[c[0] for c in SMALL])
 @pytest.mark.parametrize("seed", [0, 1])
-def test_host_ffn_matches_oracle(name, dtype, T, H, E, F, k, seed):
+@pytest.mark.parametrize("bf16_dot", [True, False], ids=["bf16dot", "widened"])
+def test_host_ffn_matches_oracle(name, dtype, T, H, E, F, k, seed, bf16_dot):
     cfg = replace(CONFIGS["c2_mixtral_decode"], name=name, dtype=dtype, tokens=T, hidden=H, experts=E, ffn=F,
                   top_k=k, n_resident=E // 2)
     L, rp, n_res, off_rows, w13, w2, dims = offloaded_case(cfg, seed)
     assert T * k - n_res > 0
-    y = moe.moe_host_ffn(dims, rp["counts"], rp["seg_start"], n_res, w13, w2, off_rows)
+    y = moe.moe_host_ffn(dims, rp["counts"], rp["seg_start"], n_res, w13, w2, off_rows, bf16_dot=bf16_dot)
     ref = expected(L, rp, n_res, cfg)
     assert y.shape == ref.shape
     assert rel_l2(y, ref) <= TOL
@@ -86,6 +95,22 @@ def test_host_ffn_thread_count_and_pinning_do_not_change_bits():
     y7 = moe.moe_host_ffn(dims, rp["counts"], rp["seg_start"], n_res, w13, w2, off_rows, threads=7)
     yp = moe.moe_host_ffn(dims, rp["counts"], rp["seg_start"], n_res, w13, w2, off_rows, pin=True)
     assert np.array_equal(y1, y7) and np.array_equal(y1, yp)
+
+
+def test_host_ffn_bf16_dot_path_is_taken_where_the_cpu_has_it():
+    """bf16 layers: the bf16 dot-product path and the widened fp32 one agree to the fp32
+    bar; where the CPU has the instruction they differ in the last bits (a different
+    summation), so the flag does switch paths."""
+    cfg = replace(CONFIGS["c2_mixtral_decode"], name="t", tokens=24, hidden=256, experts=8, ffn=192, top_k=2,
+                  n_resident=3)
+    L, rp, n_res, off_rows, w13, w2, dims = offloaded_case(cfg, 7)
+    y_dot = moe.moe_host_ffn(dims, rp["counts"], rp["seg_start"], n_res, w13, w2, off_rows, bf16_dot=True)
+    y_wide = moe.moe_host_ffn(dims, rp["counts"], rp["seg_start"], n_res, w13, w2, off_rows, bf16_dot=False)
+    assert rel_l2(y_dot, y_wide) <= TOL
+    if cpu_has_bf16_dot():
+        assert not np.array_equal(y_dot, y_wide)
+    else:
+        assert np.array_equal(y_dot, y_wide)
 
 
 def test_host_ffn_all_resident_is_a_no_op():
