@@ -332,7 +332,8 @@ moe_status moe_pack_weights(const void* src, void* dst, int64_t rows, int64_t co
     const size_t bytes = (size_t)n * (dtype == MOE_BF16 ? 2 : 4);
     const uintptr_t s0 = reinterpret_cast<uintptr_t>(src), d0 = reinterpret_cast<uintptr_t>(dst);
     if (n > 0 && s0 < d0 + bytes && d0 < s0 + bytes) return MOE_ERR_INVALID_ARG;  // overlapping buffers
-    return hip_status(saem::launch_pack_weights(src, dst, rows, cols, dtype == MOE_BF16, static_cast<hipStream_t>(stream)));
+    return hip_status(
+        saem::launch_pack_weights(src, dst, rows, cols, dtype == MOE_BF16, static_cast<hipStream_t>(stream)));
 }
 
 moe_status moe_stage_accumulate(int32_t experts, const int32_t* counts, int64_t* log, void* stream) {

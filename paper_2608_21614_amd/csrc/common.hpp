@@ -81,7 +81,9 @@ __device__ __forceinline__ Frag8<Elt> zero_frag();
 template <>
 __device__ __forceinline__ Frag8<uint16_t> zero_frag<uint16_t>() { return {zero_bf16x8()}; }
 template <>
-__device__ __forceinline__ Frag8<float> zero_frag<float>() { return {f32x4{0.f, 0.f, 0.f, 0.f}, f32x4{0.f, 0.f, 0.f, 0.f}}; }
+__device__ __forceinline__ Frag8<float> zero_frag<float>() {
+    return {f32x4{0.f, 0.f, 0.f, 0.f}, f32x4{0.f, 0.f, 0.f, 0.f}};
+}
 
 __device__ __forceinline__ f32x4 mma_frag(const Frag8<uint16_t>& a, const Frag8<uint16_t>& b, f32x4 c) {
     return mfma16x16x32(a.v, b.v, c);

@@ -11,29 +11,31 @@
 // block is 1 KB of contiguous memory whose 64 16-byte pieces are the 64 lanes'
 // MFMA A operands.
 //
-// Three kernel families:
+// Two kernel families:
 //  * stream  (T <= 64, decode, and fp32 prefill; bf16 MFMA 16x16x32, fp32 MFMA
-//    16x16x4): at decode the weights are streamed from HBM exactly once.  A workgroup owns 32 features (phase 1: 32 gate + 32 up weight
-//    rows) or 64 outputs (phase 2: 64 rows of W2) of one expert; the weights are
-//    the MFMA M side and the expert's tokens the N side, in tiles of 16.  Its
-//    four waves split K interleaved -- wave w takes the 32-wide K steps w, w+4,
-//    w+8, ... -- so at any moment the workgroup reads 4 KB of contiguous memory
-//    per weight tile; each wave double-buffers its loads in registers (the next
-//    two K steps are in flight while the MFMAs of the current two run).  The
-//    waves' partial tiles are summed through LDS in wave order.  Phase 2 also
-//    splits K across workgroups into `ks` chunks whose partial sums the combine
-//    adds in fixed order.  SwiGLU is applied in the phase-1 epilogue, so the gate
-//    and up projections are never stored.
-//  * tiled   (bf16, T > 64, prefill): one 256 x 256 output tile per workgroup
-//    (eight waves of 128 x 64 on MFMA 32x32x16), both operands read as 1 KB
-//    tile-layout blocks by direct global->LDS loads through a five-stage ring;
-//    a token gather first copies the resident groups' rows into that layout,
-//    and phase 1 writes the activations in it; the expert outputs are bf16.
-//    fp32 batches with T > 64 run the same kernel on chunks of 64 rows of a
-//    group: an item is then (group, weight rows, chunk), found from a prefix over
-//    the active groups that every workgroup computes.
-// All of them read counts and offsets from device memory: the grid is sized for
-// the worst case on the host and surplus workgroups exit at once.
+//    16x16x4): at decode the weights are streamed from HBM exactly once.  A
+//    workgroup owns 32 features (phase 1: 32 gate + 32 up weight rows) or 64
+//    outputs (phase 2: 64 rows of W2) of one expert; the weights are the MFMA
+//    M side and the expert's tokens the N side, in tiles of 16.  Its four waves
+//    split K interleaved -- wave w takes the 32-wide K steps w, w+4, w+8, ... --
+//    so at any moment the workgroup reads 4 KB of contiguous memory per weight
+//    tile; each wave double-buffers its loads in registers (the next two K
+//    steps are in flight while the MFMAs of the current two run).  The waves'
+//    partial tiles are summed through LDS in wave order.  Phase 2 also splits K
+//    across workgroups into `ks` chunks whose partial sums the combine adds in
+//    fixed order.  SwiGLU is applied in the phase-1 epilogue, so the gate and up
+//    projections are never stored.  fp32 batches with T > 64 run this kernel on
+//    chunks of 64 rows of a group: an item is then (group, weight rows, chunk),
+//    found from a prefix over the active groups that every workgroup computes.
+//  * tiled   (bf16, T > 64, prefill): 256 x 256 output tiles (eight waves of
+//    128 x 64 on MFMA 32x32x16) that one workgroup per CU works through in
+//    turn, both operands read as 1 KB tile-layout blocks by direct global->LDS
+//    loads through a five-stage ring; a token gather first copies the resident
+//    groups' rows into that layout, and phase 1 writes the activations in it;
+//    the expert outputs are bf16.
+// Both read counts and offsets from device memory: the stream kernel's grid is
+// sized for the worst case on the host and surplus workgroups exit at once; the
+// tiled kernel runs one workgroup per CU.
 #include "common.hpp"
 #include "kernels.hpp"
 
@@ -482,12 +484,13 @@ __global__ void __launch_bounds__(256) k_ffn_stream(Args a) {
 // the kernel's only LDS: kGStages - 1 slabs (128 KB) stay in flight while one is
 // multiplied, which is what the load latency under this traffic asks for.
 //
-// Items come from a table the token gather writes (one scalar load per
-// workgroup); group g owns (weight tiles) x ceil(rows / 256) items, weight tile
-// major.  The XCDs get equal contiguous ranges of the real items (the hardware
-// deals workgroups to the 8 XCDs round-robin), so the 32 CUs of an XCD work on
-// neighbouring tiles of one group and share its weight and token panels in
-// their L2.
+// Items come from a table the token gather writes (one scalar load per item);
+// group g owns (weight tiles) x ceil(rows / 256) items, weight tile major.  The
+// kernel is persistent, one workgroup per CU: the XCDs get equal contiguous
+// ranges of the real items (the hardware deals workgroups to the 8 XCDs
+// round-robin), which an XCD's workgroups take in turn, so its 32 CUs start
+// each round together on neighbouring tiles of one group and share its weight
+// and token panels in their L2.
 
 constexpr int kGM = 256;          // weight rows per item
 constexpr int kGN = 256;          // group rows (tokens) per item
@@ -683,177 +686,179 @@ __global__ void __launch_bounds__(512, 1) k_ffn_tiled(Args a, const TileItem* __
     const int xend = min((xcd + 1) * per, n_items);
     const int step = gridDim.x / 8;
     for (int item = xcd * per + (int)(blockIdx.x / 8); item < xend; item += step) {
-    __syncthreads();  // the previous item's epilogue is done with the LDS
-    const TileItem it = tab[item];
+        __syncthreads();  // the previous item's epilogue is done with the LDS
+        const TileItem it = tab[item];
 
-    const int tid = threadIdx.x, lane = lane_id();
-    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
-    const int wm = wave & 1, wn = wave >> 1;
-    const int K = kDown ? it.Fg : a.H;
-    const int nk = K / 32;  // slabs
-    const size_t wsize = (size_t)(kDown ? 1 : 2) * it.Fg * a.H;  // elements of one expert's matrix
-    const uint16_t* wbase;
-    if (it.wsel >= 0) wbase = static_cast<const uint16_t*>(kDown ? a.w2 : a.w13) + (size_t)it.wsel * wsize;
-    else wbase = static_cast<const uint16_t*>(kDown ? a.ws2 : a.ws13) + (size_t)(-it.wsel - 1) * wsize;
-    // phase 1: features r0 .. r0 + 127 (gate rows in LDS blocks 0..7, up rows in 8..15);
-    // phase 2: rows r0 .. r0 + 255 of W2
-    const int r0 = it.wt * (kDown ? kGM : kGM / 2);
-    const int rows_out = kDown ? a.H : it.Fg;  // rows (phase 2) or features (phase 1) that exist
-    const int n0 = it.n0;
+        const int tid = threadIdx.x, lane = lane_id();
+        const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+        const int wm = wave & 1, wn = wave >> 1;
+        const int K = kDown ? it.Fg : a.H;
+        const int nk = K / 32;  // slabs
+        const size_t wsize = (size_t)(kDown ? 1 : 2) * it.Fg * a.H;  // elements of one expert's matrix
+        const uint16_t* wbase;
+        if (it.wsel >= 0) wbase = static_cast<const uint16_t*>(kDown ? a.w2 : a.w13) + (size_t)it.wsel * wsize;
+        else wbase = static_cast<const uint16_t*>(kDown ? a.ws2 : a.ws13) + (size_t)(-it.wsel - 1) * wsize;
+        // phase 1: features r0 .. r0 + 127 (gate rows in LDS blocks 0..7, up rows in 8..15);
+        // phase 2: rows r0 .. r0 + 255 of W2
+        const int r0 = it.wt * (kDown ? kGM : kGM / 2);
+        const int rows_out = kDown ? a.H : it.Fg;  // rows (phase 2) or features (phase 1) that exist
+        const int n0 = it.n0;
 
-    // 16-row tile of the weight matrix held in LDS weight block b; a block past the
-    // matrix reads tile 0 instead (its rows are never stored)
-    auto row_tile = [&](int b) -> int {
-        if (kDown) {
-            const int rt = r0 / 16 + b;
-            return 16 * rt < a.H ? rt : 0;
+        // 16-row tile of the weight matrix held in LDS weight block b; a block past the
+        // matrix reads tile 0 instead (its rows are never stored)
+        auto row_tile = [&](int b) -> int {
+            if (kDown) {
+                const int rt = r0 / 16 + b;
+                return 16 * rt < a.H ? rt : 0;
+            }
+            const int f16 = r0 / 16 + (b & 7);
+            if (16 * f16 >= it.Fg) return 0;
+            return b < 8 ? f16 : it.Fg / 16 + f16;
+        };
+        // this wave's loads: weight blocks 2w, 2w + 1 and token blocks 2w, 2w + 1; a token
+        // block past the group reads the group's first block instead (never stored)
+        const uint16_t* gW0 = wbase + (size_t)row_tile(2 * wave) * nk * 512 + lane * 8;
+        const uint16_t* gW1 = wbase + (size_t)row_tile(2 * wave + 1) * nk * 512 + lane * 8;
+        const uint16_t* gX[2];
+#pragma unroll
+        for (int i = 0; i < 2; ++i) {
+            const int nb = n0 / 16 + 2 * wave + i;
+            const int blk = (16 * nb < it.count) ? nb : 0;
+            if (!kDown)
+                gX[i] = static_cast<const uint16_t*>(a.xg) + (size_t)(it.xblk + blk) * (a.H / 32) * 512 + lane * 8;
+            else
+                gX[i] = static_cast<const uint16_t*>(a.act) + (size_t)(it.ablk + blk) * (a.Fa / 32) * 512 + lane * 8;
         }
-        const int f16 = r0 / 16 + (b & 7);
-        if (16 * f16 >= it.Fg) return 0;
-        return b < 8 ? f16 : it.Fg / 16 + f16;
-    };
-    // this wave's loads: weight blocks 2w, 2w + 1 and token blocks 2w, 2w + 1; a token
-    // block past the group reads the group's first block instead (never stored)
-    const uint16_t* gW0 = wbase + (size_t)row_tile(2 * wave) * nk * 512 + lane * 8;
-    const uint16_t* gW1 = wbase + (size_t)row_tile(2 * wave + 1) * nk * 512 + lane * 8;
-    const uint16_t* gX[2];
-#pragma unroll
-    for (int i = 0; i < 2; ++i) {
-        const int nb = n0 / 16 + 2 * wave + i;
-        const int blk = (16 * nb < it.count) ? nb : 0;
-        if (!kDown)
-            gX[i] = static_cast<const uint16_t*>(a.xg) + (size_t)(it.xblk + blk) * (a.H / 32) * 512 + lane * 8;
-        else
-            gX[i] = static_cast<const uint16_t*>(a.act) + (size_t)(it.ablk + blk) * (a.Fa / 32) * 512 + lane * 8;
-    }
-    const uint32_t lds0 = (uint32_t)(uintptr_t)(lds_u8*)sbuf;
-    auto issue = [&](int kt, int stage) {
-        const uint32_t base = lds0 + stage * kGStageBytes;
-        lds_load_1k(base + (2 * wave) * 1024, gW0 + (size_t)kt * 512);
-        lds_load_1k(base + (2 * wave + 1) * 1024, gW1 + (size_t)kt * 512);
-        lds_load_1k(base + (16 + 2 * wave) * 1024, gX[0] + (size_t)kt * 512);
-        lds_load_1k(base + (17 + 2 * wave) * 1024, gX[1] + (size_t)kt * 512);
-    };
+        const uint32_t lds0 = (uint32_t)(uintptr_t)(lds_u8*)sbuf;
+        auto issue = [&](int kt, int stage) {
+            const uint32_t base = lds0 + stage * kGStageBytes;
+            lds_load_1k(base + (2 * wave) * 1024, gW0 + (size_t)kt * 512);
+            lds_load_1k(base + (2 * wave + 1) * 1024, gW1 + (size_t)kt * 512);
+            lds_load_1k(base + (16 + 2 * wave) * 1024, gX[0] + (size_t)kt * 512);
+            lds_load_1k(base + (17 + 2 * wave) * 1024, gX[1] + (size_t)kt * 512);
+        };
 
-    // operand blocks of this wave: A tile m (32 rows) = LDS weight blocks ab[m], ab[m] + 1;
-    // phase 1: m = 0, 1 gate rows, m = 2, 3 the up rows of the same features
-    int ab[4];
+        // operand blocks of this wave: A tile m (32 rows) = LDS weight blocks ab[m], ab[m] + 1;
+        // phase 1: m = 0, 1 gate rows, m = 2, 3 the up rows of the same features
+        int ab[4];
 #pragma unroll
-    for (int m = 0; m < 4; ++m) ab[m] = kDown ? 8 * wm + 2 * m : (m < 2 ? 4 * wm + 2 * m : 8 + 4 * wm + 2 * (m - 2));
-    // B tile jn (32 tokens) = token blocks 16 + 4 wn + 2 jn (+1).  Lane's 16-byte piece of a
-    // 32-row (or 32-token) operand at K step s of the slab: block + (l % 32) / 16, piece
-    // (l % 16) + 16 (2 s + l / 32)
-    const int half = (lane >> 4) & 1;
-    const int piece0 = (lane & 15) + 16 * (lane >> 5);
-    // a wave whose rows or tokens all lie past the group skips its MFMAs
-    const bool live = (n0 + 64 * wn < it.count) && (r0 + (kDown ? 128 : 64) * wm < rows_out);
+        for (int m = 0; m < 4; ++m)
+            ab[m] = kDown ? 8 * wm + 2 * m : (m < 2 ? 4 * wm + 2 * m : 8 + 4 * wm + 2 * (m - 2));
+        // B tile jn (32 tokens) = token blocks 16 + 4 wn + 2 jn (+1).  Lane's 16-byte piece of a
+        // 32-row (or 32-token) operand at K step s of the slab: block + (l % 32) / 16, piece
+        // (l % 16) + 16 (2 s + l / 32)
+        const int half = (lane >> 4) & 1;
+        const int piece0 = (lane & 15) + 16 * (lane >> 5);
+        // a wave whose rows or tokens all lie past the group skips its MFMAs
+        const bool live = (n0 + 64 * wn < it.count) && (r0 + (kDown ? 128 : 64) * wm < rows_out);
 
-    f32x16 acc[4][2];
+        f32x16 acc[4][2];
 #pragma unroll
-    for (int m = 0; m < 4; ++m)
+        for (int m = 0; m < 4; ++m)
 #pragma unroll
-        for (int jn = 0; jn < 2; ++jn) acc[m][jn] = f32x16{};
+            for (int jn = 0; jn < 2; ++jn) acc[m][jn] = f32x16{};
 
 #pragma unroll
-    for (int st = 0; st < kGStages - 1; ++st)
-        if (st < nk) issue(st, st);
+        for (int st = 0; st < kGStages - 1; ++st)
+            if (st < nk) issue(st, st);
 
-    int stage = 0;
-    for (int kt = 0; kt < nk; ++kt) {
-        // slabs issued after kt: min(kGStages - 2, nk - 1 - kt), four loads each
-        const int later = nk - 1 - kt;
-        if (later >= 3) wait_then_barrier<12>();
-        else if (later == 2) wait_then_barrier<8>();
-        else if (later == 1) wait_then_barrier<4>();
-        else wait_then_barrier<0>();
-        // every wave is past slab kt - 1: its stage may be refilled
-        if (kt + kGStages - 1 < nk) issue(kt + kGStages - 1, stage == 0 ? kGStages - 1 : stage - 1);
-        if (live) {
-            const uint8_t* sp = sbuf + stage * kGStageBytes;
+        int stage = 0;
+        for (int kt = 0; kt < nk; ++kt) {
+            // slabs issued after kt: min(kGStages - 2, nk - 1 - kt), four loads each
+            const int later = nk - 1 - kt;
+            if (later >= 3) wait_then_barrier<12>();
+            else if (later == 2) wait_then_barrier<8>();
+            else if (later == 1) wait_then_barrier<4>();
+            else wait_then_barrier<0>();
+            // every wave is past slab kt - 1: its stage may be refilled
+            if (kt + kGStages - 1 < nk) issue(kt + kGStages - 1, stage == 0 ? kGStages - 1 : stage - 1);
+            if (live) {
+                const uint8_t* sp = sbuf + stage * kGStageBytes;
 #pragma unroll
-            for (int ks = 0; ks < 2; ++ks) {
-                const int off = 16 * (piece0 + 32 * ks) + 1024 * half;
-                bf16x8 A[4], B[2];
+                for (int ks = 0; ks < 2; ++ks) {
+                    const int off = 16 * (piece0 + 32 * ks) + 1024 * half;
+                    bf16x8 A[4], B[2];
+#pragma unroll
+                    for (int m = 0; m < 4; ++m)
+                        A[m] = __builtin_bit_cast(bf16x8, *reinterpret_cast<const u32x4*>(sp + ab[m] * 1024 + off));
+#pragma unroll
+                    for (int jn = 0; jn < 2; ++jn)
+                        B[jn] = __builtin_bit_cast(
+                            bf16x8, *reinterpret_cast<const u32x4*>(sp + (16 + 4 * wn + 2 * jn) * 1024 + off));
+#pragma unroll
+                    for (int m = 0; m < 4; ++m)
+#pragma unroll
+                        for (int jn = 0; jn < 2; ++jn) acc[m][jn] = mfma32x32x16(A[m], B[jn], acc[m][jn]);
+                }
+            }
+            stage = stage == kGStages - 1 ? 0 : stage + 1;
+        }
+        // Epilogue through the (now idle) LDS ring, so that the global stores are whole
+        // rows or whole tile-layout blocks instead of 8-byte pieces of 32 token rows.
+        // Lane holds column (token) l % 32 of each 32 x 32 tile, rows 8 (v / 4) + 4 (l / 32) + v % 4.
+        __syncthreads();  // every wave is done with the last stage
+        if (!kDown) {
+            // phase 1: act = silu(gate) * up in bf16, staged in the tile layout of its 16 x 4
+            // blocks (token block tb, feature block fb at LDS block 4 tb + fb)
+#pragma unroll
+            for (int jn = 0; jn < 2; ++jn) {
+                const int nl = 64 * wn + 32 * jn + (lane & 31);  // token within the item
+#pragma unroll
+                for (int m = 0; m < 2; ++m)
+#pragma unroll
+                    for (int q = 0; q < 4; ++q) {
+                        const int fl = 64 * wm + 32 * m + 8 * q + 4 * (lane >> 5);  // feature within the item
+                        const f32x16 gv = acc[m][jn], uv = acc[m + 2][jn];
+                        u32x2 packed;
+                        packed.x = pack_bf16x2(silu(gv[4 * q]) * uv[4 * q], silu(gv[4 * q + 1]) * uv[4 * q + 1]);
+                        packed.y =
+                            pack_bf16x2(silu(gv[4 * q + 2]) * uv[4 * q + 2], silu(gv[4 * q + 3]) * uv[4 * q + 3]);
+                        const int off = ((nl >> 4) * 4 + (fl >> 5)) * 1024 + 16 * ((nl & 15) + 16 * ((fl & 31) >> 3)) +
+                                        2 * (fl & 7);
+                        *reinterpret_cast<u32x2*>(sbuf + off) = packed;
+                    }
+            }
+            __syncthreads();
+            // 64 blocks of 1 KB; a block goes out if it holds rows of the group and features that exist
+            uint16_t* act = static_cast<uint16_t*>(a.act);
+            for (int c = tid; c < 64 * 64; c += 512) {
+                const int blk = c >> 6, piece = c & 63;
+                const int tb = blk >> 2, fb = blk & 3;
+                if (n0 + 16 * tb >= it.count || r0 + 32 * fb >= it.Fg) continue;
+                const u32x4 v = *reinterpret_cast<const u32x4*>(sbuf + blk * 1024 + 16 * piece);
+                *reinterpret_cast<u32x4*>(act + ((size_t)(it.ablk + n0 / 16 + tb) * (a.Fa / 32) + r0 / 32 + fb) * 512 +
+                                          8 * piece) = v;
+            }
+        } else {
+            // phase 2: expert outputs in bf16, rounded once (the combine sums them in fp32),
+            // staged as 256 token rows of 256 outputs (pitch 264 elements)
+            constexpr int kPitch = 264;
+            uint16_t* sy = reinterpret_cast<uint16_t*>(sbuf);
+#pragma unroll
+            for (int jn = 0; jn < 2; ++jn) {
+                const int nl = 64 * wn + 32 * jn + (lane & 31);
 #pragma unroll
                 for (int m = 0; m < 4; ++m)
-                    A[m] = __builtin_bit_cast(bf16x8, *reinterpret_cast<const u32x4*>(sp + ab[m] * 1024 + off));
 #pragma unroll
-                for (int jn = 0; jn < 2; ++jn)
-                    B[jn] = __builtin_bit_cast(
-                        bf16x8, *reinterpret_cast<const u32x4*>(sp + (16 + 4 * wn + 2 * jn) * 1024 + off));
-#pragma unroll
-                for (int m = 0; m < 4; ++m)
-#pragma unroll
-                    for (int jn = 0; jn < 2; ++jn) acc[m][jn] = mfma32x32x16(A[m], B[jn], acc[m][jn]);
+                    for (int q = 0; q < 4; ++q) {
+                        const int hl = 128 * wm + 32 * m + 8 * q + 4 * (lane >> 5);
+                        const f32x16 v = acc[m][jn];
+                        u32x2 packed;
+                        packed.x = pack_bf16x2(v[4 * q], v[4 * q + 1]);
+                        packed.y = pack_bf16x2(v[4 * q + 2], v[4 * q + 3]);
+                        *reinterpret_cast<u32x2*>(sy + nl * kPitch + hl) = packed;
+                    }
+            }
+            __syncthreads();
+            // 256 rows x 32 pieces of 16 bytes; rows of the group, outputs that exist
+            for (int c = tid; c < 256 * 32; c += 512) {
+                const int nl = c >> 5, piece = c & 31;
+                const int h = r0 + 8 * piece;
+                if (n0 + nl >= it.count || h >= a.H) continue;
+                const u32x4 v = *reinterpret_cast<const u32x4*>(sy + nl * kPitch + 8 * piece);
+                *reinterpret_cast<u32x4*>(a.y16 + (size_t)(it.rowbase + n0 + nl) * a.H + h) = v;
             }
         }
-        stage = stage == kGStages - 1 ? 0 : stage + 1;
-    }
-    // Epilogue through the (now idle) LDS ring, so that the global stores are whole
-    // rows or whole tile-layout blocks instead of 8-byte pieces of 32 token rows.
-    // Lane holds column (token) l % 32 of each 32 x 32 tile, rows 8 (v / 4) + 4 (l / 32) + v % 4.
-    __syncthreads();  // every wave is done with the last stage
-    if (!kDown) {
-        // phase 1: act = silu(gate) * up in bf16, staged in the tile layout of its 16 x 4
-        // blocks (token block tb, feature block fb at LDS block 4 tb + fb)
-#pragma unroll
-        for (int jn = 0; jn < 2; ++jn) {
-            const int nl = 64 * wn + 32 * jn + (lane & 31);  // token within the item
-#pragma unroll
-            for (int m = 0; m < 2; ++m)
-#pragma unroll
-                for (int q = 0; q < 4; ++q) {
-                    const int fl = 64 * wm + 32 * m + 8 * q + 4 * (lane >> 5);  // feature within the item
-                    const f32x16 gv = acc[m][jn], uv = acc[m + 2][jn];
-                    u32x2 packed;
-                    packed.x = pack_bf16x2(silu(gv[4 * q]) * uv[4 * q], silu(gv[4 * q + 1]) * uv[4 * q + 1]);
-                    packed.y = pack_bf16x2(silu(gv[4 * q + 2]) * uv[4 * q + 2], silu(gv[4 * q + 3]) * uv[4 * q + 3]);
-                    const int off = ((nl >> 4) * 4 + (fl >> 5)) * 1024 + 16 * ((nl & 15) + 16 * ((fl & 31) >> 3)) +
-                                    2 * (fl & 7);
-                    *reinterpret_cast<u32x2*>(sbuf + off) = packed;
-                }
-        }
-        __syncthreads();
-        // 64 blocks of 1 KB; a block goes out if it holds rows of the group and features that exist
-        uint16_t* act = static_cast<uint16_t*>(a.act);
-        for (int c = tid; c < 64 * 64; c += 512) {
-            const int blk = c >> 6, piece = c & 63;
-            const int tb = blk >> 2, fb = blk & 3;
-            if (n0 + 16 * tb >= it.count || r0 + 32 * fb >= it.Fg) continue;
-            const u32x4 v = *reinterpret_cast<const u32x4*>(sbuf + blk * 1024 + 16 * piece);
-            *reinterpret_cast<u32x4*>(act + ((size_t)(it.ablk + n0 / 16 + tb) * (a.Fa / 32) + r0 / 32 + fb) * 512 +
-                                      8 * piece) = v;
-        }
-    } else {
-        // phase 2: expert outputs in bf16, rounded once (the combine sums them in fp32),
-        // staged as 256 token rows of 256 outputs (pitch 264 elements)
-        constexpr int kPitch = 264;
-        uint16_t* sy = reinterpret_cast<uint16_t*>(sbuf);
-#pragma unroll
-        for (int jn = 0; jn < 2; ++jn) {
-            const int nl = 64 * wn + 32 * jn + (lane & 31);
-#pragma unroll
-            for (int m = 0; m < 4; ++m)
-#pragma unroll
-                for (int q = 0; q < 4; ++q) {
-                    const int hl = 128 * wm + 32 * m + 8 * q + 4 * (lane >> 5);
-                    const f32x16 v = acc[m][jn];
-                    u32x2 packed;
-                    packed.x = pack_bf16x2(v[4 * q], v[4 * q + 1]);
-                    packed.y = pack_bf16x2(v[4 * q + 2], v[4 * q + 3]);
-                    *reinterpret_cast<u32x2*>(sy + nl * kPitch + hl) = packed;
-                }
-        }
-        __syncthreads();
-        // 256 rows x 32 pieces of 16 bytes; rows of the group, outputs that exist
-        for (int c = tid; c < 256 * 32; c += 512) {
-            const int nl = c >> 5, piece = c & 31;
-            const int h = r0 + 8 * piece;
-            if (n0 + nl >= it.count || h >= a.H) continue;
-            const u32x4 v = *reinterpret_cast<const u32x4*>(sy + nl * kPitch + 8 * piece);
-            *reinterpret_cast<u32x4*>(a.y16 + (size_t)(it.rowbase + n0 + nl) * a.H + h) = v;
-        }
-    }
     }
 }
 
@@ -1044,11 +1049,13 @@ hipError_t launch_grouped_ffn(const Shape& s, const FfnArgs& fa, hipStream_t st,
         a.ipg_r = s.F / 32;
         a.ipg_s = s.S > 0 ? s.Fs / 32 : 1;
         long long grid = a.ipg_r * chunks_r + a.ipg_s * chunks_s;
-        if (grid > 0) hipLaunchKernelGGL((k_ffn_stream<float, 4, false, false>), dim3((unsigned)grid), dim3(256), 0, st, a);
+        if (grid > 0)
+            hipLaunchKernelGGL((k_ffn_stream<float, 4, false, false>), dim3((unsigned)grid), dim3(256), 0, st, a);
         if (hipError_t e = mark(); e != hipSuccess) return e;
         a.ipg_r = a.ipg_s = s.H / 64;
         grid = a.ipg_r * (chunks_r + chunks_s);
-        if (grid > 0) hipLaunchKernelGGL((k_ffn_stream<float, 4, true, false>), dim3((unsigned)grid), dim3(256), 0, st, a);
+        if (grid > 0)
+            hipLaunchKernelGGL((k_ffn_stream<float, 4, true, false>), dim3((unsigned)grid), dim3(256), 0, st, a);
         return hipGetLastError();
     }
     if (use_stream(s)) {

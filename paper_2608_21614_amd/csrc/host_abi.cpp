@@ -25,7 +25,8 @@ const char* moe_status_str(moe_status s) {
         case MOE_ERR_UNSUPPORTED: return "unsupported shape or option";
         case MOE_ERR_WORKSPACE: return "workspace missing or too small";
         case MOE_ERR_HIP: return "HIP launch or runtime error";
-        case MOE_ERR_SCRATCH_LIMIT: return "layer needs more workspace than the fixed scratch array of the no-allocation entry point";
+        case MOE_ERR_SCRATCH_LIMIT:
+            return "layer needs more workspace than the fixed scratch array of the no-allocation entry point";
     }
     return "unknown status";
 }

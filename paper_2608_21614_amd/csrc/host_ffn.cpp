@@ -368,7 +368,8 @@ moe_status moe_offload_plan(int32_t experts, const int32_t* counts, const int32_
         if (resident || counts[e] <= 0) continue;
         choice[e] = 0;
         // host: stream the expert's weights from host memory, or its FLOPs, whichever is slower
-        const double t_host = std::max(r.expert_bytes / (r.host_GBps * 1e9), counts[e] * r.flops_per_pair / (r.host_GFLOPs * 1e9));
+        const double t_host =
+            std::max(r.expert_bytes / (r.host_GBps * 1e9), counts[e] * r.flops_per_pair / (r.host_GFLOPs * 1e9));
         // GPU: copy the weights over the host link, then stream them from HBM once
         const double t_gpu = r.expert_bytes / (r.link_GBps * 1e9) + r.expert_bytes / (r.gpu_GBps * 1e9);
         host_total += t_host;

@@ -17,7 +17,8 @@ namespace {
 
 // One thread moves 8 consecutive K elements of one row (elt = 2 or 4 bytes).
 template <typename T>
-__global__ void __launch_bounds__(256) k_pack(const T* __restrict__ src, T* __restrict__ dst, long long rows, long long K) {
+__global__ void __launch_bounds__(256)
+    k_pack(const T* __restrict__ src, T* __restrict__ dst, long long rows, long long K) {
     const long long nsteps = K / 32;
     const long long chunks = rows * (K / 8);  // 8-element chunks
     for (long long c = (long long)blockIdx.x * 256 + threadIdx.x; c < chunks; c += (long long)gridDim.x * 256) {

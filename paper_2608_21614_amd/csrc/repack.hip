@@ -33,7 +33,8 @@ __global__ void __launch_bounds__(NT)
 // off_rows[p - n_res] = x[perm[p] / k]; off_w[p - n_res] = topk_w[perm[p]].
 __global__ void __launch_bounds__(256)
     k_offload_pack(int T, int k, int row_bytes, const uint8_t* __restrict__ x, const float* __restrict__ topk_w,
-                   const int32_t* __restrict__ perm, const int32_t* __restrict__ n_res_p, uint8_t* __restrict__ off_rows,
+                   const int32_t* __restrict__ perm, const int32_t* __restrict__ n_res_p,
+                   uint8_t* __restrict__ off_rows,
                    float* __restrict__ off_w) {
     const int P = T * k;
     const int nres = *n_res_p;
