@@ -21,7 +21,10 @@ Prints one JSON line on stdout:
   whole-layer rooflines, stage breakdown, a shorter CPU-oracle sample) for every
   other config -- the tiny fp32 layer, the shared+routed decode batch, the
   prefill chunk (MFMA utilisation), one layer call of the stage-structured
-  trace and the Qwen3-MoE-like decode batch -- unless --only is given.
+  trace and the Qwen3-MoE-like decode batch -- unless --only is given;
+* ep_shards (per workload, unless --ep 0): each GPU's share of the layer under
+  8-way expert parallelism timed as its own call on this GPU, beside the layer
+  with every expert resident on one GPU (the cross-GPU sum is not built).
 """
 from __future__ import annotations
 
@@ -322,6 +325,122 @@ def trace_timings(seed: int, lags, detect: bool = False, persistence: float = 0.
 # roofline and a bounded CPU-oracle sample): the tiny fp32 layer, the shared+routed
 # decode batch, the prefill chunk, one layer call of the stage-structured trace, and
 # the Qwen3-MoE-like decode batch
+def _time_layer_calls(dev, steps: int, warmup: int, rotate_bytes: int = 1 << 30, max_copies: int = 32,
+                      pack_offloaded: bool = True):
+    """Mean wall time per fused call of `dev` over `steps` calls (after `warmup`), rotating
+    enough copies of its expert weights (routed and shared) that each call reads at least
+    `rotate_bytes` of other weights before its own come round again; then the mean FFN
+    phase-1 duration from the library's stage events over min(steps, 50) more calls.
+    Returns (us per call, phase-1 us, counts, weight copies)."""
+    import numpy as np
+    import torch
+    import paper_2608_21614_amd as moe
+    from paper_2608_21614_amd.device import to_host
+
+    per_copy = sum(t.numel() * t.element_size() for t in (dev.w13, dev.w2, dev.ws13, dev.ws2) if t is not None)
+    n_copies = int(min(max_copies, max(4, -(-rotate_bytes // max(per_copy, 1)))))
+    base = (dev.w13, dev.w2, dev.ws13, dev.ws2)
+    copies = [base] + [tuple(None if t is None else t.clone() for t in base) for _ in range(n_copies - 1)]
+    o = dev.alloc_outputs()
+
+    def make_args(i, events=None):
+        dev.w13, dev.w2, dev.ws13, dev.ws2 = copies[i % n_copies]
+        a = dev.args(o, pack_offloaded=pack_offloaded)
+        if events is not None:
+            a.stage_events = ctypes.cast(events, ctypes.POINTER(ctypes.c_void_p))
+        return a
+
+    plain = [make_args(i) for i in range(n_copies)]
+    hip = moe.hip_runtime()
+    hip.hipEventCreateWithFlags.argtypes = [ctypes.POINTER(ctypes.c_void_p), ctypes.c_uint]
+    hip.hipEventElapsedTime.argtypes = [ctypes.POINTER(ctypes.c_float), ctypes.c_void_p, ctypes.c_void_p]
+    hip.hipEventDestroy.argtypes = [ctypes.c_void_p]
+    nE = moe.MOE_STAGE_EVENTS
+    P1_BEFORE, P1_AFTER = 3, 4
+    n_ev = min(steps, 50)
+    evs, created = [], []
+    for _ in range(n_ev):
+        arr = (ctypes.c_void_p * nE)()
+        for j in (P1_BEFORE, P1_AFTER):
+            ev = ctypes.c_void_p()
+            assert hip.hipEventCreateWithFlags(ctypes.byref(ev), 0) == 0
+            created.append(ev.value)
+            arr[j] = ev.value
+        evs.append(arr)
+    with_ev = [make_args(i, evs[i]) for i in range(n_ev)]
+    dev.w13, dev.w2, dev.ws13, dev.ws2 = base
+    stream = torch.cuda.current_stream()
+    for i in range(warmup):
+        moe.moe_layer_forward(plain[i % n_copies], dev.ws, stream)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for i in range(steps):
+        moe.moe_layer_forward(plain[i % n_copies], dev.ws, stream)
+    torch.cuda.synchronize()
+    us = (time.perf_counter() - t0) * 1e6 / steps
+    for a in with_ev:
+        moe.moe_layer_forward(a, dev.ws, stream)
+    torch.cuda.synchronize()
+    f = ctypes.c_float()
+    p1 = []
+    for arr in evs:
+        assert hip.hipEventElapsedTime(ctypes.byref(f), arr[P1_BEFORE], arr[P1_AFTER]) == 0
+        p1.append(f.value * 1e3)
+    for e in created:
+        hip.hipEventDestroy(e)
+    counts = to_host(o["counts"])
+    del copies, plain, with_ev, o
+    return us, float(np.mean(p1)), counts, n_copies
+
+
+def ep_shard_timings(layer, n: int, steps: int, warmup: int):
+    """One GPU's share of the layer under n-way expert parallelism, each shard timed on this
+    GPU as its own fused call, beside the whole layer with every expert resident on one GPU.
+
+    Routing is replicated (every shard routes the whole batch); shard g holds a contiguous
+    block of routed expert ids and a 64-column slice of each shared expert, and packs no
+    offloaded rows (the other experts are other GPUs' work).  What one GPU cannot show is
+    left out: the cross-GPU sum of the shards' [T, H] partial outputs is neither built nor
+    timed, so the slowest shard is a lower bound on an n-GPU layer call.
+    """
+    import numpy as np
+    import torch
+    from paper_2608_21614_amd.device import DeviceLayer
+    from workloads import ExpertShard
+
+    c = layer.cfg
+    log(f"[bench] {c.name}: {n}-way expert-parallel shards")
+    whole = ExpertShard(layer, 1, 0)
+    dev = DeviceLayer(whole)
+    one_us, one_p1, counts, one_copies = _time_layer_calls(dev, steps, warmup, pack_offloaded=False)
+    del dev
+    torch.cuda.empty_cache()
+    shards = []
+    for g in range(n):
+        sh = ExpertShard(layer, n, g)
+        dev = DeviceLayer(sh)
+        us, p1, cnt, nc = _time_layer_calls(dev, steps, warmup, pack_offloaded=False)
+        del dev
+        torch.cuda.empty_cache()
+        alg = algorithmic_bytes(sh.cfg, cnt, sh.resident)
+        rec = {"shard": g, "experts": [int(sh.expert_ids[0]), int(sh.expert_ids[-1]) + 1] if sh.n_slots else [],
+               "shared_cols": list(sh.shared_cols), "pairs": alg["n_res"], "active_experts": alg["active"],
+               "us_per_call": us, "ffn_phase1_us": p1, "weight_copies": nc}
+        if c.tokens > 64:
+            rec["ffn_phase1_TFLOPs"] = alg["phase1_flops"] / (p1 * 1e-6) / 1e12
+        else:
+            rec["ffn_phase1_GBps"] = alg["phase1_bytes"] / (p1 * 1e-6) / 1e9
+        shards.append(rec)
+    t = np.array([r["us_per_call"] for r in shards])
+    return {"n": n, "split": "routed experts in contiguous id blocks; shared experts by 64-column FFN slices; "
+                             "routing replicated; no offloaded-row pack",
+            "one_gpu_all_resident_us": one_us, "one_gpu_all_resident_ffn_phase1_us": one_p1,
+            "one_gpu_weight_copies": one_copies,
+            "max_shard_us": float(t.max()), "mean_shard_us": float(t.mean()), "imbalance": float(t.max() / t.mean()),
+            "speedup_of_slowest_shard": one_us / float(t.max()),
+            "not_built": "the cross-GPU reduction of the shards' partial outputs", "shards": shards}
+
+
 OTHER_WORKLOADS = ["c1_tiny_f32", "c3_shared_decode", "c4_prefill", "c5_stage_trace", "c6_qwen3_decode",
                    "c4_prefill_f32"]
 
@@ -531,6 +650,8 @@ def measure_workload(name, cfg, args, steps: int, warmup: int, cpu_seconds: floa
         hip.hipEventDestroy(e)
     del copies, dev, o, plain, timed, diag
     torch.cuda.empty_cache()
+    if args.ep > 1:
+        m["ep_shards"] = ep_shard_timings(layer, args.ep, min(steps, 100), warmup)
     if cpu_seconds > 0:
         log(f"[bench] {name}: timing the CPU oracle ({cpu_seconds:.0f} s sample)")
         m["cpu_baseline"] = cpu_baseline(layer, cpu_seconds)
@@ -571,6 +692,10 @@ def main() -> int:
     ap.add_argument("--detect", action="store_true",
                     help="with --trace: stage boundaries from the cue machine on the generated tokens "
                          "(Section IV-B.1) instead of the trace's true stage ends")
+    ap.add_argument("--ep", type=int, default=8, metavar="N",
+                    help="also time each GPU's share of every measured workload under N-way expert parallelism "
+                         "(each shard as its own call on this GPU) beside the all-resident one-GPU call; "
+                         "extra object, 0 or 1: off")
     ap.add_argument("--calib-copy-mib", type=int, default=0,
                     help="run one plain device copy of this many MiB first (counter calibration)")
     args = ap.parse_args()
@@ -612,7 +737,7 @@ def main() -> int:
     }
     for key in ("hbm_gbps_expert_weights", "hbm_gbps_layer_algorithmic", "stages_us_instrumented",
                 "step_us_instrumented", "ms_per_step_without_events", "ms_per_step_graph", "hbm_read_probe_GBps",
-                "mfma_tflops_layer_algorithmic", "layer_roofline", "roofline", "bookkeeping", "hybrid"):
+                "mfma_tflops_layer_algorithmic", "layer_roofline", "roofline", "bookkeeping", "hybrid", "ep_shards"):
         if key in m:
             result[key] = m[key]
     if not args.only:

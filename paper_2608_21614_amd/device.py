@@ -91,12 +91,16 @@ class DeviceLayer:
         }
 
     def args(self, o: Dict[str, torch.Tensor], logits_in: bool = False, x: Optional[torch.Tensor] = None,
-             keep_intermediates: bool = True):
-        """moe_layer_args over this layer and the output buffers in ``o``."""
+             keep_intermediates: bool = True, pack_offloaded: bool = True):
+        """moe_layer_args over this layer and the output buffers in ``o``.
+
+        pack_offloaded=False leaves the offloaded-row list out (no pack), as an expert-parallel
+        shard does: the rows of experts it does not hold are another GPU's work, not the host's.
+        """
         kw = {}
         if keep_intermediates:
-            kw = {n: o[n] for n in ("topk_idx", "topk_w", "counts", "seg_start", "perm", "inv_perm", "n_res",
-                                    "off_rows", "off_w")}
+            names = ("topk_idx", "topk_w", "counts", "seg_start", "perm", "inv_perm", "n_res")
+            kw = {n: o[n] for n in names + (("off_rows", "off_w") if pack_offloaded else ())}
         return layer_args(self.dims, self.x if x is None else x, self.w_router, self.bias, self.expert_slot,
                           self.w13, self.w2, self.ws13, self.ws2, o["out"], o["out_dtype"],
                           MOE_LOGITS_IN if logits_in else 0, logits=o["logits"], **kw)

@@ -3,7 +3,8 @@
 This module only draws random inputs with the shapes, value distributions and
 routing structure of the five MoE-layer workloads (a tiny fp32 layer, a
 Mixtral-like decode layer, a fine-grained shared+routed decode layer, a
-prefill chunk, and a stage-structured decode trace).  It holds none of the
+prefill chunk, and a stage-structured decode trace) and one GPU's share of a
+layer under expert parallelism (``ExpertShard``, a view).  It holds none of the
 layer's arithmetic: no router product, no top-k, no repacking, no expert FFN,
 no combine.  Both the CPU oracle's tests and the GPU path's tests and bench
 consume the buffers it returns, so both sides see bit-identical inputs.
@@ -39,7 +40,7 @@ import numpy as np
 
 __all__ = [
     "MoEConfig", "TraceConfig", "CONFIGS", "TRACE", "SyntheticLayer", "StageTrace",
-    "bf16_bits_to_f32", "f32_to_bf16_bits", "make_layer",
+    "bf16_bits_to_f32", "f32_to_bf16_bits", "make_layer", "ExpertShard",
 ]
 
 # tags of the per-tensor random streams
@@ -293,6 +294,66 @@ class SyntheticLayer:
         for e in np.flatnonzero(self.resident):
             out[self.expert_slot[e]] = e
         return out
+
+
+class ExpertShard:
+    """One GPU's share of a layer under n-way expert parallelism (a view: no tensor is redrawn).
+
+    Routing is replicated, so every shard sees the layer's own ``x``, router and bias and
+    computes the same top-k.  The routed experts are split into n contiguous id blocks
+    (sizes as ``numpy.array_split`` gives them); shard g holds block g in slots 0.. (id
+    order) and marks every other expert absent.  Each shared expert is split by its FFN
+    columns in 64-column units (the SwiGLU acts on each column on its own, so the shards'
+    partial outputs add up to the whole layer's); a shard whose share of the columns is
+    empty holds no shared expert.
+    """
+
+    def __init__(self, layer: "SyntheticLayer", n: int, g: int):
+        c = layer.cfg
+        if not (n >= 1 and 0 <= g < n):
+            raise ValueError(f"shard {g} of {n}")
+        self.layer = layer
+        self.n, self.g = int(n), int(g)
+        ids = np.array_split(np.arange(c.experts), n)[g]
+        self.expert_ids = ids.astype(np.int32)
+        self.expert_slot = np.full(c.experts, -1, dtype=np.int32)
+        self.expert_slot[ids] = np.arange(len(ids), dtype=np.int32)
+        self.resident = self.expert_slot >= 0
+        f0 = f1 = 0
+        if c.shared > 0:
+            if c.shared_ffn % 64:
+                raise ValueError("shared FFN width must be a multiple of 64")
+            units = np.array_split(np.arange(c.shared_ffn // 64), n)[g]
+            if len(units):
+                f0, f1 = int(units[0]) * 64, (int(units[-1]) + 1) * 64
+        self.shared_cols = (f0, f1)
+        self.cfg = replace(c, shared=c.shared if f1 > f0 else 0, shared_ffn=f1 - f0, n_resident=len(ids),
+                           description=f"{c.description}; expert-parallel shard {g} of {n}: routed experts "
+                                       f"{list(ids[[0, -1]]) if len(ids) else []}, shared columns [{f0}, {f1})")
+        self.x, self.w_router, self.bias = layer.x, layer.w_router, layer.bias
+
+    @property
+    def n_slots(self) -> int:
+        return len(self.expert_ids)
+
+    def slot_experts(self) -> np.ndarray:
+        return self.expert_ids.copy()
+
+    def w13(self, e: int) -> np.ndarray:
+        return self.layer.w13(e)
+
+    def w2(self, e: int) -> np.ndarray:
+        return self.layer.w2(e)
+
+    def ws13(self, s: int) -> np.ndarray:
+        f0, f1 = self.shared_cols
+        F = self.layer.cfg.shared_ffn
+        w = self.layer.ws13(s)
+        return np.ascontiguousarray(np.concatenate([w[f0:f1], w[F + f0:F + f1]]))
+
+    def ws2(self, s: int) -> np.ndarray:
+        f0, f1 = self.shared_cols
+        return np.ascontiguousarray(self.layer.ws2(s)[:, f0:f1])
 
 
 def make_layer(tokens: int, hidden: int, experts: int, ffn: int, top_k: int, dtype: str = "bf16",
