@@ -227,8 +227,11 @@ constexpr int stream_mt(int nt) { return nt == 1 ? 2 : 4; }
 // caches for a later use), which raises the streaming rate when the call's
 // weights are far larger than the caches; small weight sets that stay in the
 // MALL between calls are read with plain loads.
+// fp32 operands double the fragment registers: the bound of two workgroups per CU keeps
+// the 64-row kernel at two waves per SIMD (without it, one); the bf16 kernels reach two
+// on their own.
 template <typename Elt, int NT, bool kDown, bool kStreamW>
-__global__ void __launch_bounds__(256) k_ffn_stream(Args a) {
+__global__ void __launch_bounds__(256, sizeof(Elt) == 4 ? 2 : 1) k_ffn_stream(Args a) {
     using F8 = Frag8<Elt>;
     constexpr int MT = stream_mt(NT);              // 16-row weight tiles per workgroup
     constexpr int MH = MT / 2;                     // phase 1: gate tiles (then as many up tiles)
