@@ -58,7 +58,8 @@ def run_shards(moe, lay, n, sample):
 
 @pytest.mark.parametrize("name,n,n_sample", [("c1_tiny_f32", 8, None), ("c2_mixtral_decode", 8, None),
                                              ("c3_shared_decode", 8, None), ("c6_qwen3_decode", 8, None),
-                                             ("c4_prefill", 8, 256), ("c3_shared_decode", 3, None)])
+                                             ("c4_prefill", 8, 256), ("c4_prefill_f32", 8, 128),
+                                             ("c3_shared_decode", 3, None)])
 def test_ep_shards_sum_to_the_whole_layer(moe, name, n, n_sample):
     lay = SyntheticLayer(CONFIGS[name], 2)
     c = lay.cfg
