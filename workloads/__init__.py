@@ -329,7 +329,8 @@ class ExpertShard:
         self.shared_cols = (f0, f1)
         self.cfg = replace(c, shared=c.shared if f1 > f0 else 0, shared_ffn=f1 - f0, n_resident=len(ids),
                            description=f"{c.description}; expert-parallel shard {g} of {n}: routed experts "
-                                       f"{list(ids[[0, -1]]) if len(ids) else []}, shared columns [{f0}, {f1})")
+                                       f"{f'[{int(ids[0])}, {int(ids[-1]) + 1})' if len(ids) else 'none'}, "
+                                       f"shared columns [{f0}, {f1})")
         self.x, self.w_router, self.bias = layer.x, layer.w_router, layer.bias
 
     @property
