@@ -321,10 +321,6 @@ def trace_timings(seed: int, lags, detect: bool = False, persistence: float = 0.
     return out
 
 
-# the configs measured besides the primary one in a default run (each with its own
-# roofline and a bounded CPU-oracle sample): the tiny fp32 layer, the shared+routed
-# decode batch, the prefill chunk, one layer call of the stage-structured trace, and
-# the Qwen3-MoE-like decode batch
 def _time_layer_calls(dev, steps: int, warmup: int, rotate_bytes: int = 1 << 30, max_copies: int = 32,
                       pack_offloaded: bool = True):
     """Mean wall time per fused call of `dev` over `steps` calls (after `warmup`), rotating
@@ -377,7 +373,7 @@ def _time_layer_calls(dev, steps: int, warmup: int, rotate_bytes: int = 1 << 30,
     for i in range(steps):
         moe.moe_layer_forward(plain[i % n_copies], dev.ws, stream)
     torch.cuda.synchronize()
-    us = (time.perf_counter() - t0) * 1e6 / steps
+    us = (time.perf_counter() - t0) * 1e6 / max(steps, 1)
     for a in with_ev:
         moe.moe_layer_forward(a, dev.ws, stream)
     torch.cuda.synchronize()
@@ -390,7 +386,7 @@ def _time_layer_calls(dev, steps: int, warmup: int, rotate_bytes: int = 1 << 30,
         hip.hipEventDestroy(e)
     counts = to_host(o["counts"])
     del copies, plain, with_ev, o
-    return us, float(np.mean(p1)), counts, n_copies
+    return us, float(np.mean(p1)) if p1 else 0.0, counts, n_copies
 
 
 def ep_shard_timings(layer, n: int, steps: int, warmup: int):
@@ -412,7 +408,7 @@ def ep_shard_timings(layer, n: int, steps: int, warmup: int):
     log(f"[bench] {c.name}: {n}-way expert-parallel shards")
     whole = ExpertShard(layer, 1, 0)
     dev = DeviceLayer(whole)
-    one_us, one_p1, counts, one_copies = _time_layer_calls(dev, steps, warmup, pack_offloaded=False)
+    one_us, one_p1, _, one_copies = _time_layer_calls(dev, steps, warmup, pack_offloaded=False)
     del dev
     torch.cuda.empty_cache()
     shards = []
@@ -441,6 +437,10 @@ def ep_shard_timings(layer, n: int, steps: int, warmup: int):
             "not_built": "the cross-GPU reduction of the shards' partial outputs", "shards": shards}
 
 
+# the configs measured besides the primary one in a default run (each with its own
+# roofline and a bounded CPU-oracle sample): the tiny fp32 layer, the shared+routed
+# decode batch, the prefill chunk, one layer call of the stage-structured trace, and
+# the Qwen3-MoE-like decode batch (and c4's shape in fp32)
 OTHER_WORKLOADS = ["c1_tiny_f32", "c3_shared_decode", "c4_prefill", "c5_stage_trace", "c6_qwen3_decode",
                    "c4_prefill_f32"]
 
