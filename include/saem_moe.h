@@ -209,7 +209,9 @@ typedef struct moe_layer_args {
      * caller created (timing enabled); the call records them on `stream`:
      * [0] before routing, [1] after routing, [2] after repacking, [3] after the
      * offloaded-row pack, [4] after FFN phase 1 (gate/up + SwiGLU), [5] after
-     * FFN phase 2 (down projection), [6] after the combine. */
+     * FFN phase 2 (down projection), [6] after the combine.  At decode (T <= 64)
+     * the repacking runs inside FFN phase 1 and the pack inside phase 2, so [2]
+     * and [3] follow [1] directly. */
     void* const* stage_events;
 } moe_layer_args;
 
@@ -217,7 +219,8 @@ typedef struct moe_layer_args {
 
 /*
  * Fused forward of one MoE layer: route -> repack (+ offloaded pack) ->
- * grouped SwiGLU FFN over resident and shared experts -> combine.  `out` holds
+ * grouped SwiGLU FFN over resident and shared experts -> combine (at decode the
+ * repacking and the pack run inside the two FFN launches).  `out` holds
  * the resident-plus-shared output; the offloaded list (off_rows, off_w,
  * perm[n_res:], n_res) is returned for host execution, whose results the caller
  * merges with moe_combine(..., y_off, ...).  Needs moe_workspace_bytes(&dims).

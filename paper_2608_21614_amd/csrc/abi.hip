@@ -270,7 +270,13 @@ static moe_status layer_forward(const moe_layer_args* a, void* ws, size_t ws_byt
         e = mark(saem::launch_route_topk(s, a->x, a->w_router, lin ? nullptr : a->bias, logits, lin, idx, w,
                                          at<float>(ws, L.part), hs),
                  1);
-    if (e == hipSuccess) e = mark(saem::launch_repack(s, idx, a->expert_slot, counts, seg, perm, inv, nres, hs), 2);
+    // decode: FFN phase 1 does the repacking itself (one launch fewer); the stage event
+    // after the repack then follows the routing directly
+    const bool fuse_repack = saem::ffn_fuses_repack(s);
+    if (e == hipSuccess)
+        e = mark(fuse_repack ? hipSuccess
+                             : saem::launch_repack(s, idx, a->expert_slot, counts, seg, perm, inv, nres, hs),
+                 2);
     if (s.T == 0) {
         for (int i = 3; i < MOE_STAGE_EVENTS && e == hipSuccess; ++i) e = mark(hipSuccess, i);
         return hip_status(e);
@@ -284,6 +290,14 @@ static moe_status layer_forward(const moe_layer_args* a, void* ws, size_t ws_byt
         f.off_w = a->off_w;
     }
     f.x = a->x; f.perm = perm; f.counts = counts; f.seg_start = seg; f.expert_slot = a->expert_slot;
+    if (fuse_repack) {
+        f.topk_idx = idx;
+        f.rp_counts = counts;
+        f.rp_seg_start = seg;
+        f.rp_perm = perm;
+        f.rp_inv_perm = inv;
+        f.rp_n_res = nres;
+    }
     f.w13 = a->w13; f.w2 = a->w2; f.ws13 = a->ws13; f.ws2 = a->ws2;
     f.act = at<char>(ws, L.act);
     f.xg = at<char>(ws, L.xg);
@@ -295,7 +309,7 @@ static moe_status layer_forward(const moe_layer_args* a, void* ws, size_t ws_byt
     f.ks = L.ks;
     f.y_ks_stride = L.rows * (long long)s.H;
     // the token gather of the bf16 prefill path (with the offloaded-row pack), or the
-    // standalone pack of the fp32 prefill path; at decode the pack is in FFN phase 1
+    // standalone pack of the fp32 prefill path; at decode the pack is in FFN phase 2
     if (e == hipSuccess)
         e = mark(fold_pack ? saem::launch_gather_tokens(s, f, hs)
                            : saem::launch_offload_pack(s, a->x, w, perm, nres, a->off_rows, a->off_w, hs), 3);

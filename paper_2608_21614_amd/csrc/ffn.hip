@@ -27,6 +27,12 @@
 //    projections are never stored.  fp32 batches with T > 64 run this kernel on
 //    chunks of 64 rows of a group: an item is then (group, weight rows, chunk),
 //    found from a prefix over the active groups that every workgroup computes.
+//    In the fused forward at decode, phase 1 also does the repacking: its
+//    workgroups count the top-k ids themselves (the batch is at most 512 pairs)
+//    and look their group's tokens up in them, one extra workgroup writes the
+//    repack's outputs for phase 2 and the combine, and phase 2's trailing
+//    workgroups pack the offloaded rows.  That saves the repack's launch and
+//    its chain of dependent memory round trips before the weights start to flow.
 //  * tiled   (bf16, T > 64, prefill): 256 x 256 output tiles (eight waves of
 //    128 x 64 on MFMA 32x32x16) that one workgroup per CU works through in
 //    turn, both operands read as 1 KB tile-layout blocks by direct global->LDS
@@ -36,6 +42,7 @@
 // Both read counts and offsets from device memory: the stream kernel's grid is
 // sized for the worst case on the host and surplus workgroups exit at once; the
 // tiled kernel runs one workgroup per CU.
+#include "block_ops.hpp"
 #include "common.hpp"
 #include "kernels.hpp"
 
@@ -62,7 +69,8 @@ struct Args {
     int ipg_r;        // items (workgroups) per routed group
     int ipg_s;        // items per shared group
     int chunked;      // stream kernel: items cover the groups' rows in chunks of 64 (fp32 prefill)
-    // offloaded-row pack done by the workgroups past the FFN items (phase 1 only)
+    // offloaded-row pack done by the workgroups past the FFN items (phase 1; phase 2
+    // in the fused path)
     const float* topk_w;
     const int32_t* n_res;
     void* off_rows;
@@ -71,6 +79,14 @@ struct Args {
     int32_t* tmeta;   // bf16 prefill: item tables of the tiled kernels
     int tcap1;        // capacity of the phase-1 table
     uint16_t* y16;    // bf16 prefill: expert outputs [rows][H] in bf16 (instead of y)
+    // decode with the repacking in phase 1 (fused): the ids, and the repack's outputs
+    int fused;
+    const int32_t* topk_idx;
+    int32_t* rp_counts;
+    int32_t* rp_seg_start;
+    int32_t* rp_perm;
+    int32_t* rp_inv_perm;
+    int32_t* rp_n_res;
 };
 
 // off_rows[p - n_res] = x[perm[p] / k] and off_w[p - n_res] = topk_w[perm[p]] for the
@@ -130,6 +146,98 @@ __device__ int list_active(const Args& a, int* s_list, int* s_wsum, int4* s_info
     const int n = s_wsum[0] + s_wsum[1] + s_wsum[2] + s_wsum[3];
     __syncthreads();
     return n;
+}
+
+// list_active for a phase-1 workgroup of the fused decode path, where no repack has
+// run yet: the counts come from the top-k ids (P = T k <= 512 pairs, two per thread,
+// ids outside [0, E) dropped), and one wave scans them in group order -- resident
+// experts by id, then offloaded ones -- into segment starts, as the repack does, and
+// compacts the active resident experts in the same pass.  The list, counts and starts
+// are the ones list_active reads after a repack.  *id0 / *id1: this thread's ids (pairs
+// tid and tid + 256, -1 past P), for group_rows_from_ids.  s_scr: 1024 ints of LDS.
+__device__ int list_active_from_ids(const Args& a, int* s_list, int4* s_info, int* s_scr, int* id0, int* id1) {
+    int* s_cnt = s_scr;         // [256] pairs per expert
+    int* s_slot = s_scr + 256;  // [256] slot of each expert (-1 past E)
+    int* s_n = s_scr + 512;     // [1] active experts
+    const int tid = threadIdx.x, wave = tid >> 6, lane = lane_id();
+    const int P = a.T * a.k;
+    s_cnt[tid] = 0;
+    s_slot[tid] = tid < a.E ? a.expert_slot[tid] : -1;
+    const int q0 = a.topk_idx[tid < P ? tid : 0], q1 = a.topk_idx[tid + 256 < P ? tid + 256 : 0];
+    *id0 = (tid < P && q0 >= 0 && q0 < a.E) ? q0 : -1;
+    *id1 = (tid + 256 < P && q1 >= 0 && q1 < a.E) ? q1 : -1;
+    __syncthreads();
+    if (*id0 >= 0) atomicAdd(&s_cnt[*id0], 1);
+    if (*id1 >= 0) atomicAdd(&s_cnt[*id1], 1);
+    __syncthreads();
+    if (wave == 0) {
+        int cnt[4], sl[4];
+        bool res[4];
+        int rs = 0, os = 0, ac = 0;  // lane owns experts 4 lane .. 4 lane + 3
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+            const int e = 4 * lane + i;
+            cnt[i] = s_cnt[e];
+            sl[i] = s_slot[e];
+            res[i] = e < a.E && is_resident(sl[i], a.slots);
+            if (res[i]) rs += cnt[i];
+            else os += cnt[i];
+            if (res[i] && cnt[i] > 0) ++ac;
+        }
+        int rinc = rs, oinc = os, ainc = ac;
+#pragma unroll
+        for (int off = 1; off < 64; off <<= 1) {
+            const int x = __shfl_up(rinc, off, 64), y = __shfl_up(oinc, off, 64), z = __shfl_up(ainc, off, 64);
+            if (lane >= off) {
+                rinc += x;
+                oinc += y;
+                ainc += z;
+            }
+        }
+        const int rtot = __shfl(rinc, 63, 64);
+        int rp = rinc - rs, op = rtot + (oinc - os), pos = ainc - ac;
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+            const int e = 4 * lane + i;
+            const int start = res[i] ? rp : op;
+            if (res[i]) rp += cnt[i];
+            else op += cnt[i];
+            if (res[i] && cnt[i] > 0) {
+                s_list[pos] = e;
+                s_info[pos] = make_int4(start, cnt[i], sl[i], 0);
+                ++pos;
+            }
+        }
+        if (lane == 63) *s_n = ainc;
+    }
+    __syncthreads();
+    return *s_n;
+}
+
+// The tokens of expert e's pairs in index order (its rows in the packed order), from the
+// ids list_active_from_ids left in registers: s_tok[n] = token of row n.  s_w8: 8 ints.
+__device__ void group_rows_from_ids(int e, int k, int id0, int id1, int* s_tok, int* s_w8) {
+    const int tid = threadIdx.x, wave = tid >> 6, lane = lane_id();
+    const unsigned long long m0 = __ballot(id0 == e), m1 = __ballot(id1 == e);
+    if (lane == 0) {
+        s_w8[wave] = __popcll(m0);
+        s_w8[4 + wave] = __popcll(m1);
+    }
+    __syncthreads();
+    int b0 = 0, b1 = 0;
+    for (int w = 0; w < 4; ++w) {
+        b1 += s_w8[w];
+        if (w < wave) {
+            b0 += s_w8[w];
+            b1 += s_w8[4 + w];
+        }
+    }
+    const unsigned long long lt = (1ull << lane) - 1ull;
+    // an expert appears at most once per token, so a group holds at most T <= 64 rows
+    const int r0 = b0 + __popcll(m0 & lt), r1 = b1 + __popcll(m1 & lt);
+    if (id0 == e && r0 < 64) s_tok[r0] = tid / k;
+    if (id1 == e && r1 < 64) s_tok[r1] = (tid + 256) / k;
+    __syncthreads();
 }
 
 // Routed group from its expert's segment start, count and slot.
@@ -237,19 +345,35 @@ __global__ void __launch_bounds__(256, sizeof(Elt) == 4 ? 2 : 1) k_ffn_stream(Ar
     constexpr int MH = MT / 2;                     // phase 1: gate tiles (then as many up tiles)
     constexpr int U = sizeof(Elt) == 2 ? 2 : 1;    // K steps per load batch (two batches in flight)
     __shared__ int s_list[256];
-    __shared__ int s_wsum[4];
+    __shared__ int s_wsum[8];
     __shared__ int4 s_info[256];
-    __shared__ f32x4 s_red[4][MT][NT][kWave];
+    // the epilogue's partial tiles; before it, the fused path's scratch (counts, segment
+    // starts, the group's token rows) or, in the repack workgroup, the repack's LDS
+    constexpr int kRedBytes = 4 * MT * NT * kWave * 16;
+    constexpr int kRepackBytes = repack_lds_ints<256>() * 4;
+    __shared__ __attribute__((aligned(16))) uint8_t s_raw[kRedBytes > kRepackBytes ? kRedBytes : kRepackBytes];
+    auto& s_red = *reinterpret_cast<f32x4 (*)[4][MT][NT][kWave]>(s_raw);
+    int* const s_scr = reinterpret_cast<int*>(s_raw);  // 1024 ints
+    int* const s_gtok = s_scr + 1024;                    // 64 rows
     __shared__ int s_ipre[kGMaxGroups + 1];
     __shared__ int s_tot;
 
     const int item = blockIdx.x;
     const int n_items = a.max_routed * a.ipg_r + a.S * a.ipg_s;
-    if (!kDown && !a.chunked && item >= n_items) {  // trailing workgroups pack the offloaded rows
-        pack_offloaded(a, item - n_items, gridDim.x - n_items, sizeof(Elt));
+    if (!a.chunked && item >= n_items) {
+        if (a.fused && !kDown) {  // the fused path's repack: one workgroup, P <= 512
+            if (item == n_items)
+                repack_chunks<256>(a.T, a.E, a.k, a.slots, 0, (a.T * a.k + 255) / 256, a.topk_idx, a.expert_slot,
+                                   a.rp_counts, a.rp_seg_start, a.rp_perm, a.rp_inv_perm, a.rp_n_res,
+                                   reinterpret_cast<int*>(s_raw));
+        } else if (a.fused == (int)kDown) {  // trailing workgroups pack the offloaded rows
+            pack_offloaded(a, item - n_items, gridDim.x - n_items, sizeof(Elt));
+        }
         return;
     }
-    const int nact = list_active(a, s_list, s_wsum, s_info);
+    int id0 = -1, id1 = -1;
+    const int nact = (a.fused && !kDown) ? list_active_from_ids(a, s_list, s_info, s_scr, &id0, &id1)
+                                         : list_active(a, s_list, s_wsum, s_info);
     // shared groups first: their items can be longer (Fs > F in phase 2), so they
     // start in the first wave of workgroups instead of forming a tail
     Group g;
@@ -289,6 +413,8 @@ __global__ void __launch_bounds__(256, sizeof(Elt) == 4 ? 2 : 1) k_ffn_stream(Ar
         const int4 info = s_info[gi];
         g = routed_group_of(a, info.x, info.y, info.z, sizeof(Elt));
         sub = i2 % a.ipg_r;
+        // fused path: the group's token rows from the ids (no perm yet)
+        if (a.fused && !kDown) group_rows_from_ids(s_list[gi], a.k, id0, id1, s_gtok, s_wsum);
     }
     if (g.count == 0) return;
 
@@ -348,7 +474,7 @@ __global__ void __launch_bounds__(256, sizeof(Elt) == 4 ? 2 : 1) k_ffn_stream(Ar
         bp[j] = nullptr;
         const int n = n0 + 16 * j + r;
         if (!kDown) {
-            const int t = group_token(a, g, n);
+            const int t = (a.fused && g.routed) ? (n < g.count ? s_gtok[n] : -1) : group_token(a, g, n);
             if (t >= 0) bp[j] = static_cast<const Elt*>(a.x) + (size_t)t * a.H + kq;
         } else if (n < g.count) {
             bp[j] = static_cast<const Elt*>(a.act) + (size_t)(g.rowbase + n) * a.Fa + kq;
@@ -943,6 +1069,8 @@ bool stream_weights(const Shape& s) {
 
 bool ffn_packs_offloaded(const Shape& s) { return use_stream(s) || s.bf16; }
 
+bool ffn_fuses_repack(const Shape& s) { return use_stream(s) && s.T > 0; }
+
 namespace {
 // bf16 prefill: row blocks of the routed groups padded to 16 rows (at most 15 pad
 // rows per group) and of the batch in order
@@ -981,6 +1109,13 @@ Args make_args(const Shape& s, const FfnArgs& fa) {
     a.tmeta = fa.tmeta;
     a.tcap1 = use_tiled(s) ? (int)tiled_items(s, false) : 0;
     a.y16 = static_cast<uint16_t*>(fa.y16);
+    a.fused = fa.topk_idx != nullptr;
+    a.topk_idx = fa.topk_idx;
+    a.rp_counts = fa.rp_counts;
+    a.rp_seg_start = fa.rp_seg_start;
+    a.rp_perm = fa.rp_perm;
+    a.rp_inv_perm = fa.rp_inv_perm;
+    a.rp_n_res = fa.rp_n_res;
     return a;
 }
 }  // namespace
@@ -1068,20 +1203,20 @@ hipError_t launch_grouped_ffn(const Shape& s, const FfnArgs& fa, hipStream_t st,
         const int mt = stream_mt(nt);
         a.ipg_r = s.F / (8 * mt);
         a.ipg_s = s.S > 0 ? s.Fs / (8 * mt) : 1;
-        int grid = a.max_routed * a.ipg_r + s.S * a.ipg_s;
-        if (fa.off_rows || fa.off_w) {
-            const int P = s.T * s.k;
-            grid += P < 64 ? P : 64;  // pack workgroups (P >= 1 here)
-        }
+        const int P = s.T * s.k;
+        const int n_pack = (fa.off_rows || fa.off_w) ? (P < 64 ? P : 64) : 0;  // pack workgroups (P >= 1)
+        // phase 1, then (fused) the repack workgroup, or the pack workgroups
+        int grid = a.max_routed * a.ipg_r + s.S * a.ipg_s + (a.fused ? 1 : n_pack);
         if (grid > 0) {
             if (s.bf16) launch_stream<uint16_t, false>(nt, sw, grid, a, st);
             else launch_stream<float, false>(nt, sw, grid, a, st);
         }
         if (hipError_t e = mark(); e != hipSuccess) return e;
-        // phase 2: 64 output rows x one K chunk per workgroup
+        // phase 2: 64 output rows x one K chunk per workgroup; (fused) then the pack
+        // workgroups, which read the perm and n_res that phase 1 wrote
         a.ipg_r = (s.H / (16 * mt)) * a.ks;
         a.ipg_s = (s.H / (16 * mt)) * a.ks;
-        grid = a.max_routed * a.ipg_r + s.S * a.ipg_s;
+        grid = a.max_routed * a.ipg_r + s.S * a.ipg_s + (a.fused ? n_pack : 0);
         if (grid > 0) {
             if (s.bf16) launch_stream<uint16_t, true>(nt, sw, grid, a, st);
             else launch_stream<float, true>(nt, sw, grid, a, st);

@@ -59,7 +59,20 @@ struct FfnArgs {
     int32_t* tmeta = nullptr;
     // bf16 prefill: phase 2 writes the expert outputs here in bf16 ([rows][H]) instead of y
     void* y16 = nullptr;
+    // decode (ffn_fuses_repack): phase 1 takes the repacking over from topk_idx. Its
+    // workgroups derive their groups from the ids, one more workgroup writes counts,
+    // seg_start, perm, inv_perm and n_res (which phase 2 and the combine read), and the
+    // offloaded rows are packed by workgroups of phase 2
+    const int32_t* topk_idx = nullptr;
+    int32_t* rp_counts = nullptr;
+    int32_t* rp_seg_start = nullptr;
+    int32_t* rp_perm = nullptr;
+    int32_t* rp_inv_perm = nullptr;
+    int32_t* rp_n_res = nullptr;
 };
+
+// True when the fused forward leaves the repacking to FFN phase 1 (decode batches).
+bool ffn_fuses_repack(const Shape& s);
 
 // True when the expert outputs are bf16 (y16) rather than fp32 partial sums (y).
 bool ffn_y_bf16(const Shape& s);
