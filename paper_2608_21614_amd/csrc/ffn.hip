@@ -154,7 +154,7 @@ __device__ int list_active(const Args& a, int* s_list, int* s_wsum, int4* s_info
 // experts by id, then offloaded ones -- into segment starts, as the repack does, and
 // compacts the active resident experts in the same pass.  The list, counts and starts
 // are the ones list_active reads after a repack.  *id0 / *id1: this thread's ids (pairs
-// tid and tid + 256, -1 past P), for group_rows_from_ids.  s_scr: 1024 ints of LDS.
+// tid and tid + 256, -1 past P), for group_rows_from_ids.  s_scr: 513 ints of LDS.
 __device__ int list_active_from_ids(const Args& a, int* s_list, int4* s_info, int* s_scr, int* id0, int* id1) {
     int* s_cnt = s_scr;         // [256] pairs per expert
     int* s_slot = s_scr + 256;  // [256] slot of each expert (-1 past E)
@@ -347,14 +347,16 @@ __global__ void __launch_bounds__(256, sizeof(Elt) == 4 ? 2 : 1) k_ffn_stream(Ar
     __shared__ int s_list[256];
     __shared__ int s_wsum[8];
     __shared__ int4 s_info[256];
-    // the epilogue's partial tiles; before it, the fused path's scratch (counts, segment
-    // starts, the group's token rows) or, in the repack workgroup, the repack's LDS
+    // the epilogue's partial tiles, or the repack's LDS in the fused path's repack
+    // workgroup (which never reaches the epilogue).  The fused prologue's scratch has
+    // its own arrays: a wave with no K steps of its own writes its partial tiles while
+    // the other waves may still read the group's token rows.
     constexpr int kRedBytes = 4 * MT * NT * kWave * 16;
     constexpr int kRepackBytes = repack_lds_ints<256>() * 4;
     __shared__ __attribute__((aligned(16))) uint8_t s_raw[kRedBytes > kRepackBytes ? kRedBytes : kRepackBytes];
     auto& s_red = *reinterpret_cast<f32x4 (*)[4][MT][NT][kWave]>(s_raw);
-    int* const s_scr = reinterpret_cast<int*>(s_raw);  // 1024 ints
-    int* const s_gtok = s_scr + 1024;                    // 64 rows
+    __shared__ int s_scr[513];  // fused prologue: pairs and slot per expert, active experts
+    __shared__ int s_gtok[64];  // fused prologue: the group's token rows
     __shared__ int s_ipre[kGMaxGroups + 1];
     __shared__ int s_tot;
 

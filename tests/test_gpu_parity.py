@@ -424,6 +424,33 @@ def test_layer_edge_shapes(moe, T, H, E, F, k, S, Fs, dtype, res):
     run_and_check_layer(moe, lay)
 
 
+@pytest.mark.parametrize("T,H,E,F,k,S,Fs,dtype,res", [
+    (4, 64, 200, 704, 7, 0, 0, "f32", 66),
+    (4, 64, 200, 704, 7, 2, 64, "f32", 66),
+    (9, 64, 60, 1408, 4, 1, 320, "bf16", 30),
+    (40, 128, 16, 192, 2, 2, 64, "bf16", 8),
+    (17, 64, 8, 64, 2, 0, 0, "f32", 4),
+])
+def test_layer_decode_few_k_steps_repeated(moe, T, H, E, F, k, S, Fs, dtype, res):
+    """Decode layers whose K (H = 64 or 128) gives some waves of the stream kernel no K
+    steps: those waves reach the epilogue first.  Ten calls of each, every one at the bar
+    (the FFN's prologue data must not share LDS with the epilogue's partial tiles)."""
+    from paper_2608_21614_amd.device import DeviceLayer
+    say("layer decode, few K steps, ten calls", T, H, E, F, k, S, Fs, dtype, res)
+    lay = make_layer(T, H, E, F, k, dtype=dtype, shared=S, shared_ffn=Fs, n_resident=res, residency="random",
+                     bias="zipf", seed=474)
+    dev, o, ref = run_and_check_layer(moe, lay)
+    first = host_f64(o["out"])
+    for _ in range(9):
+        o["out"].zero_()
+        dev.forward(o)
+        torch.cuda.synchronize()
+        got = host_f64(o["out"])
+        np.testing.assert_array_equal(got, first)  # deterministic, and every call complete
+        err = rel_l2(got[ref["sample"]], ref["out_res"])
+        assert err <= TOL[dtype]
+
+
 def test_layer_logits_in_routes_given_scores(moe):
     """MOE_LOGITS_IN: the fused forward routes caller scores, including exact ties, bit-exactly."""
     from paper_2608_21614_amd.device import DeviceLayer
