@@ -591,9 +591,17 @@ __global__ void __launch_bounds__(256, sizeof(Elt) == 4 ? 2 : 1) k_ffn_stream(Ar
 // group's rows.  Eight waves in 2 (rows) x 4 (tokens), each 128 rows x 64
 // tokens = 4 x 2 tiles of v_mfma_f32_32x32x16_bf16 (128 fp32 accumulators per
 // lane); a phase-1 wave holds the gate and the up rows of the same 64 features,
-// so SwiGLU runs in registers.  Wave w is (w % 2, w / 2), so an item whose
-// group ends within its first 128 rows still keeps one wave busy on each SIMD,
-// and a wave whose 64 tokens all lie past the group's end skips its MFMAs.
+// so SwiGLU runs in registers.  Waves 0-3 and 4-7 form two groups with one wave
+// of each on every SIMD; wave w has rows w % 2 and token quarter 2 ((w / 2) % 2)
+// + w / 4, so a group's end past its first 64 rows keeps both groups busy.  A
+// wave whose 64 tokens all lie past the group's end skips its MFMAs.
+//
+// Schedule (ping-pong): the K loop runs in half-slab phases with a barrier after
+// each.  While one wave group reads a slab's operand fragments from LDS (and
+// issues its next loads), the other multiplies the slab before, so a SIMD's
+// MFMA pipe and the CU's LDS work at once instead of every wave reading after
+// the same barrier and then multiplying (on operands already in LDS the
+// lockstep loop reaches about two thirds of the MFMA peak, this one about 0.9).
 //
 // Operands: both are read as 1 KB blocks of the MFMA tile layout (16 rows x 32
 // columns; lane l's 16 bytes are row l % 16, columns 8 (l / 16) .. + 7): the
@@ -612,8 +620,8 @@ __global__ void __launch_bounds__(256, sizeof(Elt) == 4 ? 2 : 1) k_ffn_stream(Ar
 // for all of them): each wave issues exactly four per slab and no other
 // vector-memory instruction in the K loop, so "slab kt has landed" is "at most
 // 4 x (slabs issued after kt) loads outstanding", then a barrier.  The ring is
-// the kernel's only LDS: kGStages - 1 slabs (128 KB) stay in flight while one is
-// multiplied, which is what the load latency under this traffic asks for.
+// the kernel's only LDS: up to kGStages - 1 slabs (128 KB) are in flight, which
+// is what the load latency under this traffic asks for.
 //
 // Items come from a table the token gather writes (one scalar load per item);
 // group g owns (weight tiles) x ceil(rows / 256) items, weight tile major.  The
@@ -822,7 +830,8 @@ __global__ void __launch_bounds__(512, 1) k_ffn_tiled(Args a, const TileItem* __
 
         const int tid = threadIdx.x, lane = lane_id();
         const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
-        const int wm = wave & 1, wn = wave >> 1;
+        const int grp = wave >> 2;  // wave group
+        const int wm = wave & 1, wn = 2 * ((wave >> 1) & 1) + grp;
         const int K = kDown ? it.Fg : a.H;
         const int nk = K / 32;  // slabs
         const size_t wsize = (size_t)(kDown ? 1 : 2) * it.Fg * a.H;  // elements of one expert's matrix
@@ -889,41 +898,65 @@ __global__ void __launch_bounds__(512, 1) k_ffn_tiled(Args a, const TileItem* __
 #pragma unroll
             for (int jn = 0; jn < 2; ++jn) acc[m][jn] = f32x16{};
 
+        // Phases: in phase 2 kt group 0 reads slab kt's fragments, then issues its loads of
+        // slab kt + D, while group 1 multiplies slab kt - 1; in phase 2 kt + 1 group 0
+        // multiplies slab kt while group 1 reads it and issues its loads of slab kt + D.  The
+        // barrier closing an odd phase 2 kt + 1 also waits for every wave's loads of slab kt + 1.
+        // Slab kt + D goes to the stage of slab kt - 1, which both groups have read in phases
+        // 2 kt - 2 and 2 kt - 1.  Both groups pass 2 nk + 2 barriers.
+        constexpr int D = kGStages - 1;
 #pragma unroll
-        for (int st = 0; st < kGStages - 1; ++st)
+        for (int st = 0; st < D; ++st)
             if (st < nk) issue(st, st);
-
+        auto wait_slab = [&](int n) {  // n: slabs this wave may still have in flight
+            __builtin_amdgcn_sched_barrier(0);
+            if (n >= 3) wait_then_barrier<12>();
+            else if (n == 2) wait_then_barrier<8>();
+            else if (n == 1) wait_then_barrier<4>();
+            else wait_then_barrier<0>();
+            __builtin_amdgcn_sched_barrier(0);
+        };
+        auto bar_lds = [&]() {  // end of a phase that needs no load to have landed
+            __builtin_amdgcn_sched_barrier(0);
+            asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" : : : "memory");
+            __builtin_amdgcn_sched_barrier(0);
+        };
+        wait_slab(min(D - 1, nk - 1));  // slab 0
+        if (grp == 1) bar_lds();        // phase 0: group 1 has no slab to multiply yet
         int stage = 0;
         for (int kt = 0; kt < nk; ++kt) {
-            // slabs issued after kt: min(kGStages - 2, nk - 1 - kt), four loads each
-            const int later = nk - 1 - kt;
-            if (later >= 3) wait_then_barrier<12>();
-            else if (later == 2) wait_then_barrier<8>();
-            else if (later == 1) wait_then_barrier<4>();
-            else wait_then_barrier<0>();
-            // every wave is past slab kt - 1: its stage may be refilled
-            if (kt + kGStages - 1 < nk) issue(kt + kGStages - 1, stage == 0 ? kGStages - 1 : stage - 1);
+            bf16x8 A[2][4], B[2][2];
             if (live) {
                 const uint8_t* sp = sbuf + stage * kGStageBytes;
 #pragma unroll
                 for (int ks = 0; ks < 2; ++ks) {
                     const int off = 16 * (piece0 + 32 * ks) + 1024 * half;
-                    bf16x8 A[4], B[2];
 #pragma unroll
                     for (int m = 0; m < 4; ++m)
-                        A[m] = __builtin_bit_cast(bf16x8, *reinterpret_cast<const u32x4*>(sp + ab[m] * 1024 + off));
+                        A[ks][m] = __builtin_bit_cast(bf16x8, *reinterpret_cast<const u32x4*>(sp + ab[m] * 1024 + off));
 #pragma unroll
                     for (int jn = 0; jn < 2; ++jn)
-                        B[jn] = __builtin_bit_cast(
+                        B[ks][jn] = __builtin_bit_cast(
                             bf16x8, *reinterpret_cast<const u32x4*>(sp + (16 + 4 * wn + 2 * jn) * 1024 + off));
+                }
+            }
+            if (kt + D < nk) issue(kt + D, stage == 0 ? D : stage - 1);
+            const int left = min(D - 1, nk - 2 - kt);  // slabs past kt + 1 this wave has in flight
+            if (grp == 0) bar_lds();
+            else wait_slab(left);
+            if (live) {
+#pragma unroll
+                for (int ks = 0; ks < 2; ++ks)
 #pragma unroll
                     for (int m = 0; m < 4; ++m)
 #pragma unroll
-                        for (int jn = 0; jn < 2; ++jn) acc[m][jn] = mfma32x32x16(A[m], B[jn], acc[m][jn]);
-                }
+                        for (int jn = 0; jn < 2; ++jn) acc[m][jn] = mfma32x32x16(A[ks][m], B[ks][jn], acc[m][jn]);
             }
+            if (grp == 0) wait_slab(left);
+            else bar_lds();
             stage = stage == kGStages - 1 ? 0 : stage + 1;
         }
+        if (grp == 0) bar_lds();  // phase 2 nk: group 1 multiplies the last slab
         // Epilogue through the (now idle) LDS ring, so that the global stores are whole
         // rows or whole tile-layout blocks instead of 8-byte pieces of 32 token rows.
         // Lane holds column (token) l % 32 of each 32 x 32 tile, rows 8 (v / 4) + 4 (l / 32) + v % 4.
