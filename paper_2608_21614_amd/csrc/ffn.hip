@@ -20,7 +20,9 @@
 //    split K interleaved -- wave w takes the 32-wide K steps w, w+4, w+8, ... --
 //    so at any moment the workgroup reads 4 KB of contiguous memory per weight
 //    tile; each wave double-buffers its loads in registers (the next two K
-//    steps are in flight while the MFMAs of the current two run).  The waves'
+//    steps are in flight while the MFMAs of the current two run).  In the bf16
+//    kernels a group whose rows fill one 16-row tile runs a copy of the K loop
+//    built for one tile, whatever the kernel's tile count.  The waves'
 //    partial tiles are summed through LDS in wave order.  Phase 2 also splits K
 //    across workgroups into `ks` chunks whose partial sums the combine adds in
 //    fixed order.  SwiGLU is applied in the phase-1 epilogue, so the gate and up
@@ -42,6 +44,8 @@
 // Both read counts and offsets from device memory: the stream kernel's grid is
 // sized for the worst case on the host and surplus workgroups exit at once; the
 // tiled kernel runs one workgroup per CU.
+#include <type_traits>
+
 #include "block_ops.hpp"
 #include "common.hpp"
 #include "kernels.hpp"
@@ -335,11 +339,11 @@ constexpr int stream_mt(int nt) { return nt == 1 ? 2 : 4; }
 // caches for a later use), which raises the streaming rate when the call's
 // weights are far larger than the caches; small weight sets that stay in the
 // MALL between calls are read with plain loads.
-// fp32 operands double the fragment registers: the bound of two workgroups per CU keeps
-// the 64-row kernel at two waves per SIMD (without it, one); the bf16 kernels reach two
-// on their own.
+// The bound of two workgroups per CU keeps every instance at two waves per SIMD: fp32
+// operands double the fragment registers, and the one-tile copy of the K loop (below)
+// adds registers to the wider bf16 instances; without the bound both would drop to one.
 template <typename Elt, int NT, bool kDown, bool kStreamW>
-__global__ void __launch_bounds__(256, sizeof(Elt) == 4 ? 2 : 1) k_ffn_stream(Args a) {
+__global__ void __launch_bounds__(256, 2) k_ffn_stream(Args a) {
     using F8 = Frag8<Elt>;
     constexpr int MT = stream_mt(NT);              // 16-row weight tiles per workgroup
     constexpr int MH = MT / 2;                     // phase 1: gate tiles (then as many up tiles)
@@ -465,7 +469,7 @@ __global__ void __launch_bounds__(256, sizeof(Elt) == 4 ? 2 : 1) k_ffn_stream(Ar
         }
     };
     // the first batch's weights go out before the token rows are looked up
-    F8 A0[U][MT], B0[U][NT], A1[U][MT], B1[U][NT];
+    F8 A0[U][MT], A1[U][MT];
     if (nb > 0) load_w(A0, 0);
 
     // token operand rows (N side)
@@ -483,60 +487,77 @@ __global__ void __launch_bounds__(256, sizeof(Elt) == 4 ? 2 : 1) k_ffn_stream(Ar
         }
     }
 
-    f32x4 acc[MT][NT];
-#pragma unroll
-    for (int m = 0; m < MT; ++m)
-#pragma unroll
-        for (int j = 0; j < NT; ++j) acc[m][j] = f32x4{0.f, 0.f, 0.f, 0.f};
-
-    auto load_x = [&](F8 (&B)[U][NT], int b) {
-#pragma unroll
-        for (int u = 0; u < U; ++u) {
-            const int s = sbase + 4 * (U * b + u);
-#pragma unroll
-            for (int j = 0; j < NT; ++j) B[u][j] = (j < ntile && bp[j]) ? load_frag(bp[j] + s * 32) : zero_frag<Elt>();
-        }
-    };
-    auto load = [&](F8 (&A)[U][MT], F8 (&B)[U][NT], int b) {
-        load_w(A, b);
-        load_x(B, b);
-    };
-    auto mma = [&](const F8 (&A)[U][MT], const F8 (&B)[U][NT]) {
-        // tiles past the group's last token see zero operands: no branch, fewer live registers
-#pragma unroll
-        for (int u = 0; u < U; ++u)
-#pragma unroll
-            for (int j = 0; j < NT; ++j)
-#pragma unroll
-                for (int m = 0; m < MT; ++m) acc[m][j] = mma_frag(A[u][m], B[u][j], acc[m][j]);
-    };
-    {
-        if (nb > 0) load_x(B0, 0);
-        for (int b = 0; b < nb; b += 2) {
-            if (b + 1 < nb) load(A1, B1, b + 1);
-            mma(A0, B0);
-            if (b + 2 < nb) load(A0, B0, b + 2);
-            if (b + 1 < nb) mma(A1, B1);
-        }
-    }
-    for (int i = nb * U; i < n_my; ++i) {
-        const int s = sbase + 4 * i;
-        F8 A[MT], B[NT];
+    // the K loop for NL token tiles; in the bf16 kernels a group that fills one 16-token tile
+    // runs a copy with one tile, without the MFMAs of the tiles past its end (a separate copy,
+    // not a branch in the loop, so that the two sets of accumulators never live at once).  The
+    // fp32 prefill kernel measured slower with the copy and keeps one loop.
+    auto k_loop = [&](auto nl_tag) {
+        constexpr int NL = decltype(nl_tag)::value;
+        f32x4 acc[MT][NL];
 #pragma unroll
         for (int m = 0; m < MT; ++m)
-            A[m] = kStreamW ? load_frag_stream(wp[m] + (size_t)s * 512) : load_frag(wp[m] + (size_t)s * 512);
 #pragma unroll
-        for (int j = 0; j < NT; ++j) B[j] = (j < ntile && bp[j]) ? load_frag(bp[j] + s * 32) : zero_frag<Elt>();
+            for (int j = 0; j < NL; ++j) acc[m][j] = f32x4{0.f, 0.f, 0.f, 0.f};
+
+        auto load_x = [&](F8 (&B)[U][NL], int b) {
 #pragma unroll
-        for (int j = 0; j < NT; ++j)
+            for (int u = 0; u < U; ++u) {
+                const int s = sbase + 4 * (U * b + u);
 #pragma unroll
-            for (int m = 0; m < MT; ++m) acc[m][j] = mma_frag(A[m], B[j], acc[m][j]);
-    }
+                for (int j = 0; j < NL; ++j) B[u][j] = (j < ntile && bp[j]) ? load_frag(bp[j] + s * 32) : zero_frag<Elt>();
+            }
+        };
+        auto load = [&](F8 (&A)[U][MT], F8 (&B)[U][NL], int b) {
+            load_w(A, b);
+            load_x(B, b);
+        };
+        auto mma = [&](const F8 (&A)[U][MT], const F8 (&B)[U][NL]) {
+            // tiles past the group's last token see zero operands: no branch, fewer live registers
+#pragma unroll
+            for (int u = 0; u < U; ++u)
+#pragma unroll
+                for (int j = 0; j < NL; ++j)
+#pragma unroll
+                    for (int m = 0; m < MT; ++m) acc[m][j] = mma_frag(A[u][m], B[u][j], acc[m][j]);
+        };
+        {
+            F8 B0[U][NL], B1[U][NL];
+            if (nb > 0) load_x(B0, 0);
+            // (rolled: unrolling this loop, which the lambda otherwise invites, slows the fp32 kernel)
+#pragma unroll 1
+            for (int b = 0; b < nb; b += 2) {
+                if (b + 1 < nb) load(A1, B1, b + 1);
+                mma(A0, B0);
+                if (b + 2 < nb) load(A0, B0, b + 2);
+                if (b + 1 < nb) mma(A1, B1);
+            }
+        }
+#pragma unroll 1
+        for (int i = nb * U; i < n_my; ++i) {
+            const int s = sbase + 4 * i;
+            F8 A[MT], B[NL];
+#pragma unroll
+            for (int m = 0; m < MT; ++m)
+                A[m] = kStreamW ? load_frag_stream(wp[m] + (size_t)s * 512) : load_frag(wp[m] + (size_t)s * 512);
+#pragma unroll
+            for (int j = 0; j < NL; ++j) B[j] = (j < ntile && bp[j]) ? load_frag(bp[j] + s * 32) : zero_frag<Elt>();
+#pragma unroll
+            for (int j = 0; j < NL; ++j)
+#pragma unroll
+                for (int m = 0; m < MT; ++m) acc[m][j] = mma_frag(A[m], B[j], acc[m][j]);
+        }
 
 #pragma unroll
-    for (int m = 0; m < MT; ++m)
+        for (int m = 0; m < MT; ++m)
 #pragma unroll
-        for (int j = 0; j < NT; ++j) s_red[wave][m][j][lane] = acc[m][j];
+            for (int j = 0; j < NL; ++j) s_red[wave][m][j][lane] = acc[m][j];
+    };
+    if constexpr (sizeof(Elt) == 2 && NT > 1) {
+        if (ntile == 1) k_loop(std::integral_constant<int, 1>{});
+        else k_loop(std::integral_constant<int, NT>{});
+    } else {
+        k_loop(std::integral_constant<int, NT>{});
+    }
     __syncthreads();
 
     if (!kDown) {
