@@ -377,9 +377,13 @@ __global__ void __launch_bounds__(256, 2) k_ffn_stream(Args a) {
         }
         return;
     }
-    int id0 = -1, id1 = -1;
-    const int nact = (a.fused && !kDown) ? list_active_from_ids(a, s_list, s_info, s_scr, &id0, &id1)
-                                         : list_active(a, s_list, s_wsum, s_info);
+    // a shared expert's item needs no active list (its group is known), so it starts
+    // streaming its weights without the prologue's dependent round trips
+    const bool shared_item = !a.chunked && item < a.S * a.ipg_s;
+    int id0 = -1, id1 = -1, nact = 0;
+    if (!shared_item)
+        nact = (a.fused && !kDown) ? list_active_from_ids(a, s_list, s_info, s_scr, &id0, &id1)
+                                   : list_active(a, s_list, s_wsum, s_info);
     // shared groups first: their items can be longer (Fs > F in phase 2), so they
     // start in the first wave of workgroups instead of forming a tail
     Group g;
