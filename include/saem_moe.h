@@ -48,7 +48,8 @@
  *   - Residency map: expert_slot[E] (int32, device).  Expert e is resident iff
  *     0 <= expert_slot[e] < dims.slots, and then its weights are
  *     w13[expert_slot[e]] and w2[expert_slot[e]]; any other value (e.g. -1)
- *     means offloaded.
+ *     means offloaded.  A slot holds one expert: two resident experts must not
+ *     share a slot (the FFN may then run only one of them; nothing faults).
  *   - A routed pair q = t*k + j is the j-th selected expert of token t.
  *   - Packed rows: the pairs of resident experts first, experts in ascending id,
  *     then the pairs of offloaded experts, experts in ascending id; inside an

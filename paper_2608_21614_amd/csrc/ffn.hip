@@ -85,6 +85,7 @@ struct Args {
     uint16_t* y16;    // bf16 prefill: expert outputs [rows][H] in bf16 (instead of y)
     // decode with the repacking in phase 1 (fused): the ids, and the repack's outputs
     int fused;
+    int slot_items;   // fused phase 1: routed item gi is slot gi's expert (every slot can be active)
     const int32_t* topk_idx;
     int32_t* rp_counts;
     int32_t* rp_seg_start;
@@ -159,15 +160,31 @@ __device__ int list_active(const Args& a, int* s_list, int* s_wsum, int4* s_info
 // compacts the active resident experts in the same pass.  The list, counts and starts
 // are the ones list_active reads after a repack.  *id0 / *id1: this thread's ids (pairs
 // tid and tid + 256, -1 past P), for group_rows_from_ids.  s_scr: 513 ints of LDS.
-__device__ int list_active_from_ids(const Args& a, int* s_list, int4* s_info, int* s_scr, int* id0, int* id1) {
+// The three loads it needs are PrologueIds, which a caller may issue early.
+struct PrologueIds {
+    int q0, q1, slot;  // raw top-k ids of pairs tid, tid + 256; expert_slot[tid]
+};
+__device__ __forceinline__ PrologueIds load_prologue_ids(const Args& a) {
+    const int tid = threadIdx.x, P = a.T * a.k;
+    PrologueIds p;
+    // no branch around the loads, so that a caller's later loads can stay in flight while
+    // these are waited for
+    const int sl = a.expert_slot[tid < a.E ? tid : 0];
+    p.slot = tid < a.E ? sl : -1;
+    p.q0 = a.topk_idx[tid < P ? tid : 0];
+    p.q1 = a.topk_idx[tid + 256 < P ? tid + 256 : 0];
+    return p;
+}
+__device__ int list_active_from_ids(const Args& a, const PrologueIds& ld, int* s_list, int4* s_info, int* s_scr,
+                                    int* id0, int* id1) {
     int* s_cnt = s_scr;         // [256] pairs per expert
     int* s_slot = s_scr + 256;  // [256] slot of each expert (-1 past E)
     int* s_n = s_scr + 512;     // [1] active experts
     const int tid = threadIdx.x, wave = tid >> 6, lane = lane_id();
     const int P = a.T * a.k;
     s_cnt[tid] = 0;
-    s_slot[tid] = tid < a.E ? a.expert_slot[tid] : -1;
-    const int q0 = a.topk_idx[tid < P ? tid : 0], q1 = a.topk_idx[tid + 256 < P ? tid + 256 : 0];
+    s_slot[tid] = ld.slot;
+    const int q0 = ld.q0, q1 = ld.q1;
     *id0 = (tid < P && q0 >= 0 && q0 < a.E) ? q0 : -1;
     *id1 = (tid + 256 < P && q1 >= 0 && q1 < a.E) ? q1 : -1;
     __syncthreads();
@@ -363,6 +380,7 @@ __global__ void __launch_bounds__(256, 2) k_ffn_stream(Args a) {
     __shared__ int s_gtok[64];  // fused prologue: the group's token rows
     __shared__ int s_ipre[kGMaxGroups + 1];
     __shared__ int s_tot;
+    __shared__ int s_pos;  // slot-mapped items: the slot's place in the active list
 
     const int item = blockIdx.x;
     const int n_items = a.max_routed * a.ipg_r + a.S * a.ipg_s;
@@ -377,17 +395,99 @@ __global__ void __launch_bounds__(256, 2) k_ffn_stream(Args a) {
         }
         return;
     }
-    // a shared expert's item needs no active list (its group is known), so it starts
-    // streaming its weights without the prologue's dependent round trips
+    const int wave = threadIdx.x >> 6, lane = lane_id();
+    const int r = lane & 15, kq = (lane >> 4) * 8;
+
+    // A shared expert's item needs no active list (its group is known), so it starts
+    // streaming its weights without the prologue's dependent round trips.  So does a routed
+    // item of the fused phase 1 when every slot can hold an active expert: item gi then
+    // takes slot gi, whose weights are known at once, and issues its first weight batch
+    // before the prologue finds the slot's expert, its rows and its tokens.
     const bool shared_item = !a.chunked && item < a.S * a.ipg_s;
+    const bool by_slot = !a.chunked && a.fused && !kDown && a.slot_items && !shared_item;
+    Group g;
+    int sub = 0, n0 = 0;  // n0: first row of the group this item covers
+    int slot = -1;
+    if (shared_item) {
+        g = shared_group(a, item / a.ipg_s, sizeof(Elt));
+        sub = item % a.ipg_s;
+    } else if (by_slot) {
+        const int i2 = item - a.S * a.ipg_s;
+        slot = i2 / a.ipg_r;
+        g = routed_group_of(a, 0, 0, slot, sizeof(Elt));  // rows set after the prologue
+        sub = i2 % a.ipg_r;
+        if (threadIdx.x == 0) s_pos = INT_MAX;  // read after the prologue's barriers
+    }
+
+    // weight tiles of this workgroup (16-row tiles in the tile layout) and the K chunk
+    const Elt* wp[MT];
+    int row0 = 0, kc = 0, c0 = 0, c1 = 0, n_my = 0, sbase = 0, nb = 0;
+    auto setup_weights = [&]() {
+        if (!kDown) {
+            const int f0 = sub * 16 * MH;
+            row0 = f0;
+            const int nst = a.H / 32;
+            const Elt* w = reinterpret_cast<const Elt*>(g.w13);
+#pragma unroll
+            for (int m = 0; m < MT; ++m) {
+                const int rt = (m < MH ? 0 : g.Fg / 16) + f0 / 16 + m % MH;  // gate tiles, then up tiles
+                wp[m] = w + (size_t)rt * nst * 512 + lane * 8;
+            }
+            c0 = 0;
+            c1 = nst;
+        } else {
+            const int h0 = (sub / a.ks) * 16 * MT;
+            kc = sub % a.ks;
+            row0 = h0;
+            const int nst = g.Fg / 32;
+            const Elt* w = reinterpret_cast<const Elt*>(g.w2);
+#pragma unroll
+            for (int m = 0; m < MT; ++m) wp[m] = w + (size_t)(h0 / 16 + m) * nst * 512 + lane * 8;
+            c0 = kc * nst / a.ks;
+            c1 = (kc + 1) * nst / a.ks;
+        }
+        // this wave's K steps: c0 + wave + 4 i
+        n_my = (c1 - c0 > wave) ? (c1 - c0 - wave + 3) / 4 : 0;
+        sbase = c0 + wave;
+        nb = n_my / U;
+    };
+    // batch b holds this wave's steps i = U*b .. U*b+U-1
+    auto load_w = [&](F8 (&A)[U][MT], int b) {
+#pragma unroll
+        for (int u = 0; u < U; ++u) {
+            const int s = sbase + 4 * (U * b + u);
+#pragma unroll
+            for (int m = 0; m < MT; ++m)
+                A[u][m] = kStreamW ? load_frag_stream(wp[m] + (size_t)s * 512) : load_frag(wp[m] + (size_t)s * 512);
+        }
+    };
+    F8 A0[U][MT], A1[U][MT];
+    const bool early = shared_item || by_slot;  // weights known before the prologue
     int id0 = -1, id1 = -1, nact = 0;
-    if (!shared_item)
-        nact = (a.fused && !kDown) ? list_active_from_ids(a, s_list, s_info, s_scr, &id0, &id1)
-                                   : list_active(a, s_list, s_wsum, s_info);
+    if (by_slot) {
+        // the prologue's loads first, then the weights: loads complete in order, so the ids
+        // can be used while the weight batch is still in flight.  No branch around the batch
+        // (a K step past the wave's last reads its last one; the batch is used only if nb > 0)
+        const PrologueIds ld = load_prologue_ids(a);
+        setup_weights();
+#pragma unroll
+        for (int u = 0; u < U; ++u) {
+            const int s = min(sbase + 4 * u, c1 - 1);
+#pragma unroll
+            for (int m = 0; m < MT; ++m)
+                A0[u][m] = kStreamW ? load_frag_stream(wp[m] + (size_t)s * 512) : load_frag(wp[m] + (size_t)s * 512);
+        }
+        nact = list_active_from_ids(a, ld, s_list, s_info, s_scr, &id0, &id1);
+    } else if (shared_item) {
+        setup_weights();
+        if (nb > 0) load_w(A0, 0);
+    } else if (a.fused && !kDown) {
+        nact = list_active_from_ids(a, load_prologue_ids(a), s_list, s_info, s_scr, &id0, &id1);
+    } else {
+        nact = list_active(a, s_list, s_wsum, s_info);
+    }
     // shared groups first: their items can be longer (Fs > F in phase 2), so they
     // start in the first wave of workgroups instead of forming a tail
-    Group g;
-    int sub, n0 = 0;  // n0: first row of the group this item covers
     if (a.chunked) {
         // group gi (the S shared groups, then the active routed ones) owns
         // ipg x ceil(rows / 16 NT) items, the chunks of one weight slice adjacent
@@ -413,10 +513,17 @@ __global__ void __launch_bounds__(256, 2) k_ffn_stream(Args a) {
             const int4 info = s_info[lo - a.S];
             g = routed_group_of(a, info.x, info.y, info.z, sizeof(Elt));
         }
-    } else if (item < a.S * a.ipg_s) {
-        g = shared_group(a, item / a.ipg_s, sizeof(Elt));
-        sub = item % a.ipg_s;
-    } else {
+    } else if (by_slot) {
+        // the slot's place in the active list (the lowest, should two experts share a slot)
+        for (int p = threadIdx.x; p < nact; p += 256)
+            if (s_info[p].z == slot) atomicMin(&s_pos, p);
+        __syncthreads();
+        const int pos = s_pos;
+        if (pos == INT_MAX) return;  // no active expert holds the slot
+        const int4 info = s_info[pos];
+        g = routed_group_of(a, info.x, info.y, info.z, sizeof(Elt));
+        group_rows_from_ids(s_list[pos], a.k, id0, id1, s_gtok, s_wsum);
+    } else if (!shared_item) {
         const int i2 = item - a.S * a.ipg_s;
         const int gi = i2 / a.ipg_r;
         if (gi >= nact) return;
@@ -427,54 +534,11 @@ __global__ void __launch_bounds__(256, 2) k_ffn_stream(Args a) {
         if (a.fused && !kDown) group_rows_from_ids(s_list[gi], a.k, id0, id1, s_gtok, s_wsum);
     }
     if (g.count == 0) return;
-
-    const int wave = threadIdx.x >> 6, lane = lane_id();
-    const int r = lane & 15, kq = (lane >> 4) * 8;
-
-    // weight tiles of this workgroup (16-row tiles in the tile layout) and the K chunk
-    const Elt* wp[MT];
-    int row0, kc = 0, c0, c1;
-    if (!kDown) {
-        const int f0 = sub * 16 * MH;
-        row0 = f0;
-        const int nst = a.H / 32;
-        const Elt* w = reinterpret_cast<const Elt*>(g.w13);
-#pragma unroll
-        for (int m = 0; m < MT; ++m) {
-            const int rt = (m < MH ? 0 : g.Fg / 16) + f0 / 16 + m % MH;  // gate tiles, then up tiles
-            wp[m] = w + (size_t)rt * nst * 512 + lane * 8;
-        }
-        c0 = 0;
-        c1 = nst;
-    } else {
-        const int h0 = (sub / a.ks) * 16 * MT;
-        kc = sub % a.ks;
-        row0 = h0;
-        const int nst = g.Fg / 32;
-        const Elt* w = reinterpret_cast<const Elt*>(g.w2);
-#pragma unroll
-        for (int m = 0; m < MT; ++m) wp[m] = w + (size_t)(h0 / 16 + m) * nst * 512 + lane * 8;
-        c0 = kc * nst / a.ks;
-        c1 = (kc + 1) * nst / a.ks;
+    if (!early) {
+        setup_weights();
+        // the first batch's weights go out before the token rows are looked up
+        if (nb > 0) load_w(A0, 0);
     }
-    // this wave's K steps: c0 + wave + 4 i
-    const int n_my = (c1 - c0 > wave) ? (c1 - c0 - wave + 3) / 4 : 0;
-    const int sbase = c0 + wave;
-
-    const int nb = n_my / U;
-    // batch b holds this wave's steps i = U*b .. U*b+U-1
-    auto load_w = [&](F8 (&A)[U][MT], int b) {
-#pragma unroll
-        for (int u = 0; u < U; ++u) {
-            const int s = sbase + 4 * (U * b + u);
-#pragma unroll
-            for (int m = 0; m < MT; ++m)
-                A[u][m] = kStreamW ? load_frag_stream(wp[m] + (size_t)s * 512) : load_frag(wp[m] + (size_t)s * 512);
-        }
-    };
-    // the first batch's weights go out before the token rows are looked up
-    F8 A0[U][MT], A1[U][MT];
-    if (nb > 0) load_w(A0, 0);
 
     // token operand rows (N side)
     const int ntile = min(NT, (g.count - n0 + 15) / 16);
@@ -1170,6 +1234,8 @@ Args make_args(const Shape& s, const FfnArgs& fa) {
     a.tcap1 = use_tiled(s) ? (int)tiled_items(s, false) : 0;
     a.y16 = static_cast<uint16_t*>(fa.y16);
     a.fused = fa.topk_idx != nullptr;
+    // every slot can hold an active expert: the fused phase 1 maps routed items to slots
+    a.slot_items = (s.T * s.k >= s.slots && s.E >= s.slots) ? 1 : 0;
     a.topk_idx = fa.topk_idx;
     a.rp_counts = fa.rp_counts;
     a.rp_seg_start = fa.rp_seg_start;
