@@ -425,6 +425,24 @@ def test_layer_edge_shapes(moe, T, H, E, F, k, S, Fs, dtype, res):
 
 
 @pytest.mark.parametrize("T,H,E,F,k,S,Fs,dtype,res", [
+    (8, 128, 64, 192, 4, 0, 0, "bf16", 32),    # T k = slots: routed items map to slots
+    (4, 64, 32, 128, 8, 1, 64, "bf16", 32),    # every expert resident, most slots idle
+    (16, 128, 64, 128, 4, 0, 0, "f32", 64),    # E = slots = T k
+    (2, 128, 64, 192, 4, 1, 64, "bf16", 16),   # T k < slots: items follow the active list
+    (3, 64, 40, 64, 5, 0, 0, "f32", 20),       # T k < slots, fp32
+])
+def test_layer_decode_slot_mapping(moe, T, H, E, F, k, S, Fs, dtype, res):
+    """The fused decode forward maps routed items to residency slots when every slot can
+    hold an active expert (T k >= slots), and to the active list otherwise; slots whose
+    expert gets no token exit.  Both mappings, at the layer bar, over two seeds."""
+    for seed in (0, 1):
+        say("layer decode, slot mapping", T, H, E, F, k, S, Fs, dtype, res, "seed", seed)
+        lay = make_layer(T, H, E, F, k, dtype=dtype, shared=S, shared_ffn=Fs, n_resident=res, residency="random",
+                         bias="zipf", seed=seed + 5 * T + E)
+        run_and_check_layer(moe, lay)
+
+
+@pytest.mark.parametrize("T,H,E,F,k,S,Fs,dtype,res", [
     (4, 64, 200, 704, 7, 0, 0, "f32", 66),
     (4, 64, 200, 704, 7, 2, 64, "f32", 66),
     (9, 64, 60, 1408, 4, 1, 320, "bf16", 30),
