@@ -21,8 +21,8 @@
 //    so at any moment the workgroup reads 4 KB of contiguous memory per weight
 //    tile; each wave double-buffers its loads in registers (the next two K
 //    steps are in flight while the MFMAs of the current two run).  In the bf16
-//    kernels a group whose rows fill one 16-row tile runs a copy of the K loop
-//    built for one tile, whatever the kernel's tile count.  The waves'
+//    kernels a group whose rows fill one or two 16-row tiles runs a copy of the
+//    K loop built for that many, whatever the kernel's tile count.  The waves'
 //    partial tiles are summed through LDS in wave order.  Phase 2 also splits K
 //    across workgroups into `ks` chunks whose partial sums the combine adds in
 //    fixed order.  SwiGLU is applied in the phase-1 epilogue, so the gate and up
@@ -555,10 +555,10 @@ __global__ void __launch_bounds__(256, 2) k_ffn_stream(Args a) {
         }
     }
 
-    // the K loop for NL token tiles; in the bf16 kernels a group that fills one 16-token tile
-    // runs a copy with one tile, without the MFMAs of the tiles past its end (a separate copy,
-    // not a branch in the loop, so that the two sets of accumulators never live at once).  The
-    // fp32 prefill kernel measured slower with the copy and keeps one loop.
+    // the K loop for NL token tiles; in the bf16 kernels a group that fills one or two
+    // 16-token tiles runs a copy with that many, without the MFMAs of the tiles past its end
+    // (separate copies, not a branch in the loop, so that their accumulators never live at
+    // once).  The fp32 prefill kernel measured slower with a copy and keeps one loop.
     auto k_loop = [&](auto nl_tag) {
         constexpr int NL = decltype(nl_tag)::value;
         f32x4 acc[MT][NL];
@@ -622,6 +622,7 @@ __global__ void __launch_bounds__(256, 2) k_ffn_stream(Args a) {
     };
     if constexpr (sizeof(Elt) == 2 && NT > 1) {
         if (ntile == 1) k_loop(std::integral_constant<int, 1>{});
+        else if (NT > 2 && ntile == 2) k_loop(std::integral_constant<int, 2>{});
         else k_loop(std::integral_constant<int, NT>{});
     } else {
         k_loop(std::integral_constant<int, NT>{});
