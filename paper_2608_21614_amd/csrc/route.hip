@@ -4,7 +4,7 @@
 // Scores run on MFMA (v_mfma_f32_16x16x32_bf16, or v_mfma_f32_16x16x4_f32 for
 // fp32 inputs): router rows are the M side, 16 tokens the N side.
 //
-//  * T > 64 (prefill): k_route_topk, 16 tokens per 1024-thread workgroup whose
+//  * T > 64 (prefill): k_route_topk, 8 tokens per 1024-thread workgroup whose
 //    16 waves split K and add their partial tiles in a fixed order.
 // The top-k takes one wave per token (topk_block: k rounds of a wave argmax).
 //  * T <= 64 (decode): k_router_partial spreads the scores over one workgroup
@@ -19,6 +19,10 @@
 namespace saem {
 namespace {
 
+// Tokens per workgroup: 8 of the 16-token MFMA tile, so that a 2048-token batch fills all
+// 256 CUs (every workgroup streams the whole router matrix, whatever its token count).
+constexpr int kRouteRows = 8;
+
 template <bool kBf16>
 __global__ void __launch_bounds__(kFrontThreads)
     k_route_topk(int T, int H, int E, int k, const void* __restrict__ x, const void* __restrict__ wr,
@@ -28,16 +32,17 @@ __global__ void __launch_bounds__(kFrontThreads)
     __shared__ float s_red[kFrontWaves * 16 * kScoreChunk];
     __shared__ float s_selv[64 * 8];
     __shared__ int s_sele[64 * 8];
-    const int t0 = blockIdx.x * 16;
+    const int t0 = blockIdx.x * kRouteRows;
+    const int tend = min(T, t0 + kRouteRows);  // the MFMA tile's rows past it stay zero
     if (!logits_in) {
         if (kBf16)
-            router_scores_mfma<uint16_t, 1, kFrontWaves>(T, H, E, static_cast<const uint16_t*>(x),
+            router_scores_mfma<uint16_t, 1, kFrontWaves>(tend, H, E, static_cast<const uint16_t*>(x),
                                                          static_cast<const uint16_t*>(wr), bias, t0, s_lg, s_red);
         else
-            router_scores_mfma<float, 1, kFrontWaves>(T, H, E, static_cast<const float*>(x),
+            router_scores_mfma<float, 1, kFrontWaves>(tend, H, E, static_cast<const float*>(x),
                                                       static_cast<const float*>(wr), bias, t0, s_lg, s_red);
     }
-    const int rows = min(16, T - t0);
+    const int rows = tend - t0;
     // scores <-> global, coalesced
     for (int idx = threadIdx.x; idx < rows * E; idx += kFrontThreads) {
         const int row = idx / E, e = idx % E;
@@ -238,7 +243,7 @@ hipError_t launch_route_topk(const Shape& s, const void* x, const void* w_router
     if (s.T == 0) return hipSuccess;
     if (front_small_fits(s)) return launch_small(s, x, w_router, bias, logits, logits_in, topk_idx, topk_w, part, st);
     const int li = logits_in ? 1 : 0;
-    dim3 grid((s.T + 15) / 16), block(kFrontThreads);
+    dim3 grid((s.T + kRouteRows - 1) / kRouteRows), block(kFrontThreads);
     if (s.bf16)
         hipLaunchKernelGGL(k_route_topk<true>, grid, block, 0, st, s.T, s.H, s.E, s.k, x, w_router, bias, logits, li,
                            topk_idx, topk_w);

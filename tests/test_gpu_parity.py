@@ -402,7 +402,7 @@ EDGE = [
     (100, 64, 8, 128, 2, 1, 64, "f32", 4),
     (2, 4096, 8, 14336, 2, 0, 0, "bf16", 4),
     # a prefill batch one token past a 2048 multiple: the last 256-token tile, the last
-    # 16-token router workgroup and the last 1024-pair repack chunk are all ragged
+    # 8-token router workgroup and the last 1024-pair repack chunk are all ragged
     (2049, 128, 64, 192, 6, 1, 64, "bf16", 40),
     (2049, 64, 8, 64, 2, 0, 0, "f32", 6),
     # the ABI's limits at once: 256 experts, top-8, eight shared experts
