@@ -914,9 +914,12 @@ __global__ void __launch_bounds__(512, 1) k_ffn_tiled(Args a, const TileItem* __
     const int xcd = blockIdx.x % 8;
     const int xend = min((xcd + 1) * per, n_items);
     const int step = gridDim.x / 8;
-    for (int item = xcd * per + (int)(blockIdx.x / 8); item < xend; item += step) {
+    int item = xcd * per + (int)(blockIdx.x / 8);
+    TileItem nxt = tab[item < xend ? item : 0];  // the next item's descriptor, loaded one item ahead
+    for (; item < xend; item += step) {
         __syncthreads();  // the previous item's epilogue is done with the LDS
-        const TileItem it = tab[item];
+        const TileItem it = nxt;
+        if (item + step < xend) nxt = tab[item + step];
 
         const int tid = threadIdx.x, lane = lane_id();
         const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
