@@ -138,7 +138,7 @@ __global__ void __launch_bounds__(256)
 
 // The same merge when the expert outputs come in bf16 (one chunk): 8 columns per
 // thread, so that every row load is 16 bytes; workgroup = one token x 2048 columns.
-template <bool kOutBf16>
+template <bool kOutBf16, bool kOff>
 __global__ void __launch_bounds__(256)
     k_combine_y16(int T, int H, int E, int k, int S, int slots, const int32_t* __restrict__ topk_idx,
                   const float* __restrict__ topk_w, const int32_t* __restrict__ inv_perm,
@@ -170,7 +170,7 @@ __global__ void __launch_bounds__(256)
         if (j < k && e[j] >= 0 && e[j] < E && p[j] >= 0 && p[j] < P) {
             const bool res = n_res_p ? p[j] < nres : is_resident(expert_slot[e[j]], slots);
             if (res) src[j] = 1;
-            else if (y_off && p[j] >= nres) src[j] = 2;
+            else if (kOff && p[j] >= nres) src[j] = 2;
         }
     }
     // every load first (a contribution that does not apply reads row 0 and is dropped)
@@ -180,7 +180,7 @@ __global__ void __launch_bounds__(256)
     for (int j = 0; j < kK; ++j) {
         const size_t off = (size_t)(src[j] == 1 ? p[j] : 0) * H + h;
         v[j] = *reinterpret_cast<const u32x4*>(y16 + off);
-        if (src[j] == 2) {
+        if (kOff && src[j] == 2) {
             const float* r = y_off + (size_t)(p[j] - nres) * H + h;
             vo[j][0] = *reinterpret_cast<const f32x4*>(r);
             vo[j][1] = *reinterpret_cast<const f32x4*>(r + 4);
@@ -196,7 +196,7 @@ __global__ void __launch_bounds__(256)
         if (src[j] == 1) {
             lo += w[j] * bf16x4_to_f32(u32x2{v[j].x, v[j].y});
             hi += w[j] * bf16x4_to_f32(u32x2{v[j].z, v[j].w});
-        } else if (src[j] == 2) {
+        } else if (kOff && src[j] == 2) {
             lo += w[j] * vo[j][0];
             hi += w[j] * vo[j][1];
         }
@@ -234,9 +234,13 @@ hipError_t launch_combine_ks(dim3 grid, const Shape& s, const int32_t* topk_idx,
     hipLaunchKernelGGL((k_combine<kOutBf16, KS>), grid, dim3(256), 0, st, s.T, s.H, s.E, s.k, s.S, s.slots,      \
                        topk_idx, topk_w, inv_perm, expert_slot, static_cast<const float*>(y), ks, stride, y_off,   \
                        n_res, out)
-    if (y_bf16)
-        hipLaunchKernelGGL((k_combine_y16<kOutBf16>), dim3(s.T, (s.H + 2047) / 2048), dim3(256), 0, st, s.T, s.H,
-                           s.E, s.k, s.S, s.slots, topk_idx, topk_w, inv_perm, expert_slot,
+    if (y_bf16 && y_off)
+        hipLaunchKernelGGL((k_combine_y16<kOutBf16, true>), dim3(s.T, (s.H + 2047) / 2048), dim3(256), 0, st, s.T,
+                           s.H, s.E, s.k, s.S, s.slots, topk_idx, topk_w, inv_perm, expert_slot,
+                           static_cast<const uint16_t*>(y), y_off, n_res, out);
+    else if (y_bf16)  // no offloaded outputs given: a copy without their registers (higher occupancy)
+        hipLaunchKernelGGL((k_combine_y16<kOutBf16, false>), dim3(s.T, (s.H + 2047) / 2048), dim3(256), 0, st, s.T,
+                           s.H, s.E, s.k, s.S, s.slots, topk_idx, topk_w, inv_perm, expert_slot,
                            static_cast<const uint16_t*>(y), y_off, n_res, out);
     else if (ks <= 1) SAEM_COMBINE(1);
     else if (ks <= 2) SAEM_COMBINE(2);
