@@ -138,6 +138,8 @@ __global__ void __launch_bounds__(256)
 
 // The same merge when the expert outputs come in bf16 (one chunk): 8 columns per
 // thread, so that every row load is 16 bytes; workgroup = one token x 2048 columns.
+// kOff: the caller gave the offloaded rows' outputs (y_off); without them the kernel
+// holds no registers for those rows.
 template <bool kOutBf16, bool kOff>
 __global__ void __launch_bounds__(256)
     k_combine_y16(int T, int H, int E, int k, int S, int slots, const int32_t* __restrict__ topk_idx,
